@@ -1,0 +1,27 @@
+"""Oracle for the DSI verification step -- TEST INFRASTRUCTURE ONLY.
+
+A plain, slow, fp64 CPU statement of what the verification step computes:
+the target forward over a window of k drafted tokens against a cached prefix
+(``forward64``) and the lossless accept/reject of those drafts (``verify64``),
+plus exact enumerations that pin the accept/reject rule (``bruteforce``).
+
+Only the tests, the smoke check and the CPU-baseline leg of the benchmark may
+import this package.  It shares no code with the HIP path and imports nothing
+from it; the product path never calls it.
+
+Parity status of each function (what pins it) is listed in its docstring.
+Architecture choices of the forward (RMSNorm, rotate-half RoPE, GQA head
+grouping, SwiGLU, untied head) are not fixed by the paper, which treats the
+target LM as a black box (Appendix B); they are pinned here only by invariants
+and textbook special cases -- "parity unpinned" beyond those.
+"""
+from .model import (bf16_round64, rmsnorm64, rope64, attention64, silu64,
+                        layer64, head64, forward64, embed64)
+from .verification import VerifyResult, softmax64, verify64, verify64_batch
+from . import bruteforce
+
+__all__ = [
+    "bf16_round64", "rmsnorm64", "rope64", "attention64", "silu64", "layer64",
+    "head64", "forward64", "embed64", "VerifyResult", "softmax64", "verify64",
+    "verify64_batch", "bruteforce",
+]

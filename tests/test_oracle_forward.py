@@ -1,0 +1,211 @@
+"""Pins of the fp64 forward oracle against library routines, closed forms and
+invariants (CPU only).  The architecture itself is not fixed by the paper
+(Appendix B treats the LM as a black box); these pins check that the oracle
+computes the Llama-style decoder it states, and the cache semantics of a
+verification window (k+1 prompts batched after a cached prefix, Section 2)."""
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+import dsi_synth as S
+from oracle import (bf16_round64, rmsnorm64, rope64, attention64, silu64,
+                    forward64, layer64, head64, embed64)
+
+
+def getter(shape, seed=0):
+    cache = {}
+
+    def get(layer, name):
+        key = (layer, name)
+        if key not in cache:
+            cache[key] = S.weight(shape, seed, layer, name).astype(np.float64)
+        return cache[key]
+    return get
+
+
+# ---------------------------------------------------------------- bf16 rounding
+def test_bf16_round_matches_torch_cast():
+    rng = np.random.default_rng(1)
+    x = np.concatenate([rng.standard_normal(20000) * 10.0 ** rng.integers(-6, 6, 20000),
+                        [0.0, -0.0, 1.0, -3.5]]).astype(np.float32)
+    ref = torch.from_numpy(x).to(torch.bfloat16).to(torch.float64).numpy()
+    assert np.array_equal(bf16_round64(x.astype(np.float64)), ref)
+
+
+def test_bf16_round_ties_to_even():
+    # spacing of bf16 just above 1 is 2^-7; both ties go to the even mantissa
+    assert bf16_round64(1.0 + 2.0 ** -8) == 1.0
+    assert bf16_round64(1.0 + 3 * 2.0 ** -8) == 1.0 + 2.0 ** -6
+    assert bf16_round64(-(1.0 + 3 * 2.0 ** -8)) == -(1.0 + 2.0 ** -6)
+    # fp64 inputs between fp32 values: rounding is direct, not via fp32
+    x = 1.0 + 2.0 ** -8 + 2.0 ** -40
+    assert bf16_round64(x) == 1.0 + 2.0 ** -7
+
+
+# ---------------------------------------------------------------------- RMSNorm
+def test_rmsnorm_matches_torch():
+    rng = np.random.default_rng(2)
+    x = rng.standard_normal((7, 96))
+    g = 1.0 + 0.1 * rng.standard_normal(96)
+    ref = F.rms_norm(torch.from_numpy(x), (96,), torch.from_numpy(g), eps=1e-5).numpy()
+    np.testing.assert_allclose(rmsnorm64(x, g, 1e-5), ref, rtol=1e-13, atol=1e-13)
+
+
+def test_rmsnorm_scale_invariant_and_constant_vector():
+    rng = np.random.default_rng(3)
+    x = rng.standard_normal((3, 64))
+    g = rng.standard_normal(64)
+    np.testing.assert_allclose(rmsnorm64(x * 1e3, g, 0.0), rmsnorm64(x, g, 0.0), rtol=1e-12)
+    a = -2.5
+    y = rmsnorm64(np.full((1, 8), a), np.ones(8), 1e-5)
+    np.testing.assert_allclose(y, a / np.sqrt(a * a + 1e-5), rtol=1e-15)
+
+
+# ------------------------------------------------------------------------- RoPE
+def test_rope_is_complex_rotation():
+    rng = np.random.default_rng(4)
+    T, H, hd, base = 5, 3, 16, 10000.0
+    x = rng.standard_normal((T, H, hd))
+    pos = np.array([0, 1, 7, 100, 4097])
+    out = rope64(x, pos, base)
+    half = hd // 2
+    zc = x[..., :half] + 1j * x[..., half:]
+    theta = base ** (-np.arange(0, hd, 2) / hd)
+    rot = zc * np.exp(1j * pos[:, None, None] * theta[None, None, :])
+    np.testing.assert_allclose(out[..., :half], rot.real, atol=1e-12)
+    np.testing.assert_allclose(out[..., half:], rot.imag, atol=1e-12)
+
+
+def test_rope_identity_at_zero_norm_preserving_relative():
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal((1, 2, 32))
+    np.testing.assert_array_equal(rope64(x, [0], 10000.0), x)
+    y = rope64(np.repeat(x, 3, axis=0), [3, 50, 999], 10000.0)
+    np.testing.assert_allclose(np.linalg.norm(y, axis=-1), np.linalg.norm(np.repeat(x, 3, 0), axis=-1), rtol=1e-13)
+    q, k = rng.standard_normal((2, 1, 1, 32))
+    d1 = np.sum(rope64(q, [10], 1e4) * rope64(k, [4], 1e4))
+    d2 = np.sum(rope64(q, [106], 1e4) * rope64(k, [100], 1e4))
+    assert abs(d1 - d2) < 1e-11
+
+
+# -------------------------------------------------------------------- attention
+def test_attention_matches_torch_sdpa_gqa():
+    rng = np.random.default_rng(6)
+    T, S_, Hq, Hkv, hd = 4, 9, 6, 2, 8
+    q = rng.standard_normal((T, Hq, hd))
+    k = rng.standard_normal((S_, Hkv, hd))
+    v = rng.standard_normal((S_, Hkv, hd))
+    q_pos = np.arange(5, 9)
+    k_pos = np.arange(S_)
+    out = attention64(q, k, v, q_pos, k_pos)
+    G = Hq // Hkv
+    kt = torch.from_numpy(k).repeat_interleave(G, dim=1).permute(1, 0, 2)
+    vt = torch.from_numpy(v).repeat_interleave(G, dim=1).permute(1, 0, 2)
+    qt = torch.from_numpy(q).permute(1, 0, 2)
+    mask = torch.from_numpy(k_pos[None, :] <= q_pos[:, None])
+    ref = F.scaled_dot_product_attention(qt, kt, vt, attn_mask=mask).permute(1, 0, 2).numpy()
+    np.testing.assert_allclose(out, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_attention_single_key_and_equal_scores():
+    rng = np.random.default_rng(7)
+    v = rng.standard_normal((3, 1, 4))
+    q = rng.standard_normal((1, 1, 4))
+    k = rng.standard_normal((3, 1, 4))
+    out = attention64(q, k, v, [0], [0, 1, 2])        # only key 0 visible
+    np.testing.assert_allclose(out[0, 0], v[0, 0], rtol=1e-15)
+    out = attention64(np.zeros((1, 1, 4)), k, v, [2], [0, 1, 2])   # equal scores
+    np.testing.assert_allclose(out[0, 0], v[:, 0].mean(0), rtol=1e-14)
+
+
+def test_silu_matches_torch():
+    x = np.linspace(-30, 30, 1001)
+    np.testing.assert_allclose(silu64(x), F.silu(torch.from_numpy(x)).numpy(), rtol=1e-14, atol=1e-300)
+
+
+# --------------------------------------------------------------- whole forward
+@pytest.mark.parametrize("shape_name", ["ragged_bf16", "ragged_f32", "tiny"])
+def test_cached_equals_uncached(shape_name):
+    s = S.SHAPES[shape_name]
+    get = getter(s)
+    toks = S.prefix_tokens(s, 0, 0, 23)
+    full, _ = forward64(s, get, toks)
+    _, cache = forward64(s, get, toks[:17])
+    win, cache2 = forward64(s, get, toks[17:], cache=cache)
+    np.testing.assert_allclose(win, full[17:], rtol=1e-12, atol=1e-12)
+    assert cache2[0][0].shape[0] == 23
+
+
+def test_causality():
+    s = S.SHAPES["ragged_bf16"]
+    get = getter(s)
+    toks = S.prefix_tokens(s, 0, 0, 12)
+    a, _ = forward64(s, get, toks)
+    toks2 = toks.copy()
+    toks2[9] = (toks2[9] + 1) % s.vocab
+    b, _ = forward64(s, get, toks2)
+    np.testing.assert_array_equal(a[:9], b[:9])
+    assert np.abs(a[9:] - b[9:]).max() > 1e-3
+
+
+def test_gqa_equals_mha_with_repeated_kv_heads():
+    s = S.SHAPES["gqa_hd64"]
+    G = s.n_heads // s.n_kv_heads
+    get = getter(s)
+    mha = S.Shape("mha_of_gqa", s.n_layers, s.d_model, s.n_heads, s.n_heads, s.head_dim,
+                  s.d_ff, s.vocab, gains=s.gains)
+
+    def get_mha(layer, name):
+        w = get(layer, name)
+        if name in ("wk", "wv"):
+            w = w.reshape(s.n_kv_heads, s.head_dim, s.d_model)
+            w = np.repeat(w, G, axis=0).reshape(s.n_heads * s.head_dim, s.d_model)
+        return w
+    toks = S.prefix_tokens(s, 0, 0, 10)
+    a, _ = forward64(s, get, toks)
+    b, _ = forward64(mha, get_mha, toks)
+    np.testing.assert_allclose(a, b, rtol=1e-11, atol=1e-11)
+
+
+def test_residual_wiring_with_zero_blocks():
+    """With wo = 0 and w_down = 0 every layer is the identity on the residual
+    stream, so the logits are head(rmsnorm(E[w]))."""
+    s = S.SHAPES["ragged_f32"]
+    get = getter(s)
+
+    def get0(layer, name):
+        w = get(layer, name)
+        return np.zeros_like(w) if name in ("wo", "w_down") else w
+    toks = S.prefix_tokens(s, 0, 0, 6)
+    z, _ = forward64(s, get0, toks)
+    E = get(-1, "embed")[toks]
+    ref = rmsnorm64(E, get(-1, "final_norm"), s.rms_eps) @ get(-1, "lm_head").T
+    np.testing.assert_allclose(z, ref, rtol=1e-13, atol=1e-13)
+
+
+def test_bf16_kv_rounding_is_applied_to_cache_rows():
+    s = S.SHAPES["ragged_bf16"]
+    get = getter(s)
+    toks = S.prefix_tokens(s, 0, 0, 8)
+    _, cache = forward64(s, get, toks)
+    for K, Vv in cache:
+        assert np.array_equal(bf16_round64(K), K)
+        assert np.array_equal(bf16_round64(Vv), Vv)
+    sf = S.SHAPES["ragged_f32"]
+    _, cf = forward64(sf, getter(sf), S.prefix_tokens(sf, 0, 0, 8))
+    assert not np.array_equal(bf16_round64(cf[0][0]), cf[0][0])
+
+
+def test_layer_by_layer_equals_forward():
+    s = S.SHAPES["ragged_bf16"]
+    get = getter(s)
+    toks = S.prefix_tokens(s, 0, 0, 9)
+    z, cache, hid = forward64(s, get, toks, return_hidden=True)
+    x = embed64(get, toks)
+    np.testing.assert_array_equal(x, hid[0])
+    for l in range(s.n_layers):
+        x, kn, vn = layer64(s, get, l, hid[l], np.arange(9))
+        np.testing.assert_array_equal(x, hid[l + 1])
+        np.testing.assert_array_equal(kn, cache[l][0])
+    np.testing.assert_array_equal(head64(s, get, hid[-1]), z)

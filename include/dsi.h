@@ -1,0 +1,200 @@
+/*
+ * dsi.h -- C ABI of the MI355X verification step of distributed speculative
+ * inference (DSI, arXiv 2405.14105).
+ *
+ * The paper's data-parallel step (Section 2, "Speculative Inference"): a
+ * drafter proposes k tokens; the target model receives the k+1 prompts
+ * x'_{<=i}, i = 0..k, as ONE batch, computes their k+1 logit rows, and from
+ * them emits between 1 and k+1 tokens with a lossless accept/reject rule.
+ * Each target server keeps its own KV cache and synchronises at every
+ * rejection (Section 3.1, "KV cache").  DSI's orchestration of many such
+ * verification tasks (Algorithm 1, speculation parallelism) is host-level
+ * work above this ABI; on one GPU, concurrent verification tasks are a batch
+ * of independent windows.
+ *
+ * Conventions
+ *  - All functions return dsi_status; no C++ exception crosses the ABI.  On
+ *    error, dsi_last_error() returns a thread-local message.
+ *  - Host-side validation runs before anything is enqueued: a call that
+ *    returns an error has no side effects.
+ *  - Pointers named d_* are device pointers owned by the caller; the library
+ *    never keeps them past the call.  The library owns weights, KV buffers
+ *    and its own workspaces.
+ *  - Work is enqueued on the stream given to dsi_model_create (a hipStream_t,
+ *    NULL = the null stream) and is asynchronous unless stated otherwise.
+ *  - Data-dependent errors found on the device (a token id outside [0, V),
+ *    q(d) not positive and finite) make the affected window output
+ *    n = -1, token = -1, leave its KV length unchanged, and make the next
+ *    synchronising call (dsi_sync, dsi_kv_length) return DSI_EINVAL.
+ *  - A dsi_model is immutable after its tensors are set and may be shared by
+ *    several dsi_kv; a dsi_kv and its model's stream are single-threaded.
+ */
+#ifndef DSI_H
+#define DSI_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  DSI_OK = 0,
+  DSI_EINVAL = 1,     /* invalid argument, or a device-detected input error */
+  DSI_ENOMEM = 2,     /* device allocation failed */
+  DSI_EHIP = 3,       /* HIP runtime error */
+  DSI_ECAPACITY = 4,  /* the KV cache of a window would overflow max_len */
+  DSI_ESTATE = 5      /* call out of order (e.g. a tensor was never set) */
+} dsi_status;
+
+typedef enum { DSI_F32 = 0, DSI_BF16 = 1 } dsi_dtype;
+
+/* Verification rule.
+ * DSI_SAMPLE: lossless rejection sampling -- accept d_i iff u_i < p_i(d_i)/q_i(d_i);
+ *   after the first rejection draw from norm(max(0, p - q)), after k
+ *   acceptances draw the bonus token from p_{k+1} (the rule the paper adopts
+ *   from its cited works, Sections 2 and 3.1).
+ * DSI_GREEDY: exact match against the target's argmax (Algorithm 1, the
+ *   terminate / j* steps), ties to the lowest token id. */
+typedef enum { DSI_SAMPLE = 0, DSI_GREEDY = 1 } dsi_mode;
+
+/* Decoder shape.  The paper treats the target LM as a black box
+ * (Appendix B); this library implements a Llama-style decoder: pre-norm
+ * RMSNorm, rotate-half RoPE, causal GQA attention (query head h reads KV
+ * head h / (n_heads / n_kv_heads)), SwiGLU FFN, final RMSNorm, untied head.
+ * Requirements: head_dim a multiple of 32 and at most 128; d_model a
+ * multiple of 32; n_heads a multiple of n_kv_heads. */
+typedef struct {
+  int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ff, vocab;
+  float rope_base;   /* e.g. 10000 */
+  float rms_eps;     /* e.g. 1e-5 */
+  int32_t wdtype;    /* dsi_dtype of every weight tensor */
+  int32_t kvdtype;   /* dsi_dtype of the KV cache */
+} dsi_config;
+
+typedef struct dsi_model dsi_model;  /* opaque, library-owned */
+typedef struct dsi_kv dsi_kv;        /* opaque, library-owned */
+
+/* Tensor ids for dsi_model_set_tensor.  Matrices are [out, in] row-major in
+ * the model's wdtype (bf16 as raw uint16 bit patterns); norm gains are [d].
+ *   global (layer = -1): EMBED [V, d], FINAL_NORM [d], LM_HEAD [V, d]
+ *   per layer: ATTN_NORM [d], WQ [n_heads*hd, d], WK/WV [n_kv_heads*hd, d],
+ *              WO [d, n_heads*hd], FFN_NORM [d], W_GATE/W_UP [d_ff, d],
+ *              W_DOWN [d, d_ff] */
+enum {
+  DSI_T_EMBED = 0, DSI_T_FINAL_NORM = 1, DSI_T_LM_HEAD = 2,
+  DSI_T_ATTN_NORM = 3, DSI_T_WQ = 4, DSI_T_WK = 5, DSI_T_WV = 6, DSI_T_WO = 7,
+  DSI_T_FFN_NORM = 8, DSI_T_W_GATE = 9, DSI_T_W_UP = 10, DSI_T_W_DOWN = 11
+};
+
+/* Largest number of window rows B*(k+1) one dsi_verify / dsi_accept call
+ * may carry. */
+#define DSI_MAX_ROWS 64
+
+/* Create a model with device storage for every weight (zero until set).
+ * stream: hipStream_t used by every call on this model and its KV caches. */
+dsi_status dsi_model_create(const dsi_config* cfg, void* stream, dsi_model** out);
+
+/* Upload one tensor (host memory if src_on_device == 0, else device memory).
+ * nbytes must equal the tensor's element count times the wdtype size.
+ * Matrices are re-laid out on the device into the library's streaming tile
+ * order.  Synchronous with respect to the host. */
+dsi_status dsi_model_set_tensor(dsi_model* m, int32_t layer, int32_t tensor_id,
+                                const void* src, size_t nbytes, int32_t src_on_device);
+
+/* Frees the model.  Any dsi_kv created from it must be destroyed first. */
+dsi_status dsi_model_destroy(dsi_model* m);
+
+/* KV cache for n_windows independent windows of up to max_len positions each
+ * (the per-server cache of Section 3.1, one per concurrent verification
+ * task).  Lengths start at 0 and live on the device. */
+dsi_status dsi_kv_create(dsi_model* m, int32_t n_windows, int32_t max_len, dsi_kv** out);
+dsi_status dsi_kv_destroy(dsi_kv* kv);
+
+/* Append n prompt tokens (d_tokens [n], device) to a window: runs the target
+ * over them in chunks, writes their K/V, and advances the window length by n.
+ * d_last_logits (nullable, device [V] fp32) receives the logits of the last
+ * token.  Fails with DSI_ECAPACITY if length + n may exceed max_len. */
+dsi_status dsi_prefill(dsi_model* m, dsi_kv* kv, int32_t window, const int32_t* d_tokens,
+                       int32_t n, float* d_last_logits);
+
+/* One batched verification of n_windows windows window0 .. window0+B-1.
+ * Window b has cached length L_b; its k+1 rows are (w0, d_1..d_k) at
+ * positions L_b .. L_b+k, where w0 is the last committed token that is not
+ * yet cached.  Row i attends to positions [0, L_b + i].
+ *   d_tokens [B][k+1] int32: w0, d_1..d_k
+ *   d_q      [B][k][V] fp32: drafter distributions q_1..q_k (sample mode;
+ *            may be NULL in greedy mode).  Used as given, not renormalised.
+ *   d_u      [B][k+1] fp32 in [0,1): u_1..u_k for acceptance, u_{k+1} for the
+ *            single residual/bonus draw (sample mode; NULL in greedy mode)
+ *   temperature > 0: p = softmax(z / temperature) (ignored in greedy mode)
+ *   commit: if nonzero, window lengths become L_b + n_b + 1 (w0 and the
+ *            accepted drafts stay cached; rows of rejected drafts are dead)
+ *   d_logits_out (nullable) [B*(k+1)][V] fp32: the target logits
+ *   d_hidden_out (nullable, diagnostics) [n_layers+1][B*(k+1)][d_model] fp32:
+ *            the residual stream entering each layer and entering the head
+ * Outputs (device): d_n_accepted [B] = n_b in [0, k] and d_next_token [B] =
+ * the correction (n_b < k) or bonus (n_b = k) token; the window emits
+ * d_1..d_{n_b}, next_token (Section 2: between 1 and k+1 tokens).
+ * Numerics: fp32-accurate activations against bf16 weights, KV stored in
+ * kvdtype, fp32 logits, fp64 accept/reject arithmetic. */
+typedef struct {
+  int32_t window0, n_windows, k;
+  const int32_t* d_tokens;
+  const float* d_q;
+  const float* d_u;
+  float temperature;
+  int32_t mode;      /* dsi_mode */
+  int32_t commit;
+  float* d_logits_out;
+  float* d_hidden_out;
+} dsi_verify_args;
+
+dsi_status dsi_verify(dsi_model* m, dsi_kv* kv, const dsi_verify_args* args,
+                      int32_t* d_n_accepted, int32_t* d_next_token);
+
+/* The accept/reject step alone, on caller-provided logits
+ * d_logits [B*(k+1)][V] fp32 (window-major rows); other arguments as in
+ * dsi_verify.  Uses a library workspace on the current device; calls that
+ * overlap on one device must be serialised by the caller. */
+dsi_status dsi_accept(void* stream, int32_t n_windows, int32_t k, int32_t vocab,
+                      const float* d_logits, const int32_t* d_tokens, const float* d_q,
+                      const float* d_u, float temperature, int32_t mode,
+                      int32_t* d_n_accepted, int32_t* d_next_token);
+
+/* Roll a window back to new_len (DSI terminates the threads that built on a
+ * rejected token, Algorithm 1; their cache rows become dead).  Stream-ordered;
+ * new_len must be >= 0 and not above the window's current length (checked on
+ * the device: otherwise the length is unchanged and the next synchronising
+ * call returns DSI_EINVAL). */
+dsi_status dsi_kv_rollback(dsi_kv* kv, int32_t window, int32_t new_len);
+
+/* Current length of a window.  Synchronises the stream. */
+dsi_status dsi_kv_length(dsi_kv* kv, int32_t window, int32_t* len);
+
+/* Synchronise the model's stream and report device-detected input errors
+ * (DSI_EINVAL, clearing them) or DSI_OK. */
+dsi_status dsi_sync(dsi_model* m);
+
+/* Copy positions [0, len) of one window and layer out of (export) or into
+ * (import) the cache, as K [n_kv_heads][len][head_dim] and
+ * V [n_kv_heads][len][head_dim] in kvdtype.  d_k / d_v are device buffers.
+ * Diagnostics and tests only; stream-ordered.  Import does not change the
+ * window length. */
+dsi_status dsi_kv_export(dsi_kv* kv, int32_t window, int32_t layer, int32_t len,
+                         void* d_k, void* d_v);
+dsi_status dsi_kv_import(dsi_kv* kv, int32_t window, int32_t layer, int32_t len,
+                         const void* d_k, const void* d_v);
+
+/* Set a window's length directly (after dsi_kv_import).  Stream-ordered. */
+dsi_status dsi_kv_set_length(dsi_kv* kv, int32_t window, int32_t len);
+
+/* Thread-local description of the last error. */
+const char* dsi_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DSI_H */

@@ -1,0 +1,265 @@
+// Causal window-over-prefix attention with grouped KV heads, split over key
+// chunks, plus the log-sum-exp combine of the chunk partials.
+//
+// Row i of window b (position L_b + i) attends to keys [0, L_b + i]: the
+// cached prefix and the window rows before it (the k+1 prompts of one
+// verification, Section 2).  For one (window, KV head) the G = n_heads /
+// n_kv query heads times R window rows form the query side; they are cut
+// into tiles of 16 queries.  Per 32-key step a wavefront computes
+//   S^T[key][query] = K . Q^T     (A = 16 K rows, B = Q^T hi/lo)
+//   O^T[d][query]  += V^T . P^T   (A = V^T rows of the transposed cache)
+// with 16x16x32 bf16 MFMAs (two per product for the hi/lo query or
+// probability split), so every operand is a 16-byte lane load and the
+// query owned by a lane (l % 16) is the same in S^T, P^T and O^T: the
+// online-softmax rescale is lane-local.  The K rows of the two S^T tiles are
+// permuted so that lane l ends up holding keys p0 + 8*(l/16) + 0..7, which is
+// exactly its P^T B-operand fragment.  fp32 caches use 16x16x4 fp32 MFMAs
+// on the same data arrangement.
+#include <math.h>
+
+#include "device_util.h"
+
+namespace dsi {
+
+namespace {
+
+template <int KVB, int HD>
+__global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
+  constexpr int DS = HD / 32;
+  constexpr int DT = HD / 16;
+  __shared__ float sm[4][16];
+  __shared__ float sl[4][16];
+  __shared__ f32x4 so[4][DT][64];
+
+  const int lane = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+  const int c = blockIdx.x, y = blockIdx.y, z = blockIdx.z;
+  const int win = z / a.n_kv, kvh = z % a.n_kv;
+  const int G = a.n_heads / a.n_kv;
+  const int R = a.rows.rows_per_window;
+  const int wabs = a.rows.window0 + win;
+  const int len = a.rows.lens[wabs];
+  const int klen = len + R;
+  const int c0 = c * a.chunk;
+  const int c1 = min(klen, c0 + a.chunk);
+
+  const int qi = y * 16 + (lane & 15);
+  const bool qvalid = qi < G * R;
+  const int gh = qvalid ? qi / R : 0;
+  const int ri = qvalid ? qi % R : 0;
+  const int qpos = qvalid ? len + ri : -1;
+  const int mtok = win * R + ri;
+  const int head = kvh * G + gh;
+
+  // query fragments (B operand of S^T): Q[q][ds*32 + 8*(l/16) + e]
+  const float* qrow = a.q + (size_t)mtok * (a.n_heads * HD) + head * HD;
+  bf16x8 qh[DS], ql[DS];
+  F8 qf[DS];
+#pragma unroll
+  for (int ds = 0; ds < DS; ++ds) {
+    const int d0 = ds * 32 + (lane >> 4) * 8;
+    F8 v;
+    if (qvalid) {
+      v.a = *(const float4*)(qrow + d0);
+      v.b = *(const float4*)(qrow + d0 + 4);
+    } else {
+      v.a = v.b = float4{0.f, 0.f, 0.f, 0.f};
+    }
+    if (KVB) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        uint16_t h, l2;
+        split_bf16(f8_get(v, e), h, l2);
+        qh[ds][e] = __builtin_bit_cast(__bf16, h);
+        ql[ds][e] = __builtin_bit_cast(__bf16, l2);
+      }
+    } else {
+      qf[ds] = v;
+    }
+  }
+
+  float mrun = -INFINITY, lrun = 0.f;
+  f32x4 o[DT];
+#pragma unroll
+  for (int t = 0; t < DT; ++t) o[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const size_t kbase = ((size_t)wabs * a.n_kv + kvh) * (size_t)a.maxlen * HD;
+  const size_t vbase = ((size_t)wabs * a.n_kv + kvh) * (size_t)HD * a.maxlen;
+  const int r16 = lane & 15;
+  const int kgrp = (lane >> 4) * 8;
+
+  for (int p0 = c0 + 32 * w; p0 < c1; p0 += 128) {
+    f32x4 st[2];
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      st[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+      const int key = p0 + (r16 >> 2) * 8 + t * 4 + (r16 & 3);
+#pragma unroll
+      for (int ds = 0; ds < DS; ++ds) {
+        const size_t kidx = kbase + (size_t)key * HD + ds * 32 + kgrp;
+        if (KVB) {
+          const u32x4 kv = *(const u32x4*)((const uint16_t*)a.kc + kidx);
+          const bf16x8 kb = as_bf16x8(kv);
+          st[t] = mfma_bf16(kb, qh[ds], st[t]);
+          st[t] = mfma_bf16(kb, ql[ds], st[t]);
+        } else {
+          F8 kf;
+          kf.a = *(const float4*)((const float*)a.kc + kidx);
+          kf.b = *(const float4*)((const float*)a.kc + kidx + 4);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) st[t] = mfma_f32(f8_get(kf, e), f8_get(qf[ds], e), st[t]);
+        }
+      }
+    }
+    // lane holds keys p0 + kgrp + (t*4 + j) for query (lane & 15)
+    float sv[8];
+    float mloc = -INFINITY;
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int key = p0 + kgrp + t * 4 + j;
+        const float v = st[t][j] * a.scale;
+        const float vm = (key <= qpos && key < c1) ? v : -INFINITY;
+        sv[t * 4 + j] = vm;
+        mloc = fmaxf(mloc, vm);
+      }
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+    const float mnew = fmaxf(mrun, mloc);
+    const float base = (mnew == -INFINITY) ? 0.f : mnew;
+    const float alpha = expf(mrun - base);
+    float pv[8];
+    float lsum = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      pv[e] = expf(sv[e] - base);
+      lsum += pv[e];
+    }
+    lrun = lrun * alpha + lsum;
+    mrun = mnew;
+#pragma unroll
+    for (int t = 0; t < DT; ++t) o[t] *= alpha;
+
+    if (KVB) {
+      bf16x8 ph, pl;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        uint16_t h, l2;
+        split_bf16(pv[e], h, l2);
+        ph[e] = __builtin_bit_cast(__bf16, h);
+        pl[e] = __builtin_bit_cast(__bf16, l2);
+      }
+#pragma unroll
+      for (int t = 0; t < DT; ++t) {
+        const size_t vidx = vbase + (size_t)(t * 16 + r16) * a.maxlen + p0 + kgrp;
+        const bf16x8 vv = as_bf16x8(*(const u32x4*)((const uint16_t*)a.vc + vidx));
+        o[t] = mfma_bf16(vv, ph, o[t]);
+        o[t] = mfma_bf16(vv, pl, o[t]);
+      }
+    } else {
+#pragma unroll
+      for (int t = 0; t < DT; ++t) {
+        const size_t vidx = vbase + (size_t)(t * 16 + r16) * a.maxlen + p0 + kgrp;
+        F8 vf;
+        vf.a = *(const float4*)((const float*)a.vc + vidx);
+        vf.b = *(const float4*)((const float*)a.vc + vidx + 4);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[t] = mfma_f32(f8_get(vf, e), pv[e], o[t]);
+      }
+    }
+  }
+
+  // combine the four waves of this workgroup
+  lrun += __shfl_xor(lrun, 16);
+  lrun += __shfl_xor(lrun, 32);
+  if (lane < 16) {
+    sm[w][lane] = mrun;
+    sl[w][lane] = lrun;
+  }
+#pragma unroll
+  for (int t = 0; t < DT; ++t) so[w][t][lane] = o[t];
+  __syncthreads();
+  const size_t zyc = ((size_t)z * a.n_qtiles + y) * a.n_chunks + c;
+  for (int it = threadIdx.x; it < DT * 64; it += 256) {
+    const int t = it >> 6, l = it & 63, q = l & 15;
+    float M = fmaxf(fmaxf(sm[0][q], sm[1][q]), fmaxf(sm[2][q], sm[3][q]));
+    const float b = (M == -INFINITY) ? 0.f : M;
+    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ww = 0; ww < 4; ++ww) acc += so[ww][t][l] * expf(sm[ww][q] - b);
+    float* dst = a.part_o + (zyc * 16 + q) * HD + t * 16 + (l >> 4) * 4;
+    *(float4*)dst = float4{acc[0], acc[1], acc[2], acc[3]};
+  }
+  if (threadIdx.x < 16) {
+    const int q = threadIdx.x;
+    float M = fmaxf(fmaxf(sm[0][q], sm[1][q]), fmaxf(sm[2][q], sm[3][q]));
+    const float b = (M == -INFINITY) ? 0.f : M;
+    float L = 0.f;
+#pragma unroll
+    for (int ww = 0; ww < 4; ++ww) L += sl[ww][q] * expf(sm[ww][q] - b);
+    a.part_ml[zyc * 16 + q] = make_float2(M, L);
+  }
+}
+
+template <int HD>
+__global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a) {
+  const int y = blockIdx.x, z = blockIdx.y;
+  const int win = z / a.n_kv, kvh = z % a.n_kv;
+  const int G = a.n_heads / a.n_kv;
+  const int R = a.rows.rows_per_window;
+  const size_t zy = (size_t)z * a.n_qtiles + y;
+  for (int it = threadIdx.x; it < 16 * HD; it += 256) {
+    const int q = it / HD, d = it % HD;
+    const int qi = y * 16 + q;
+    if (qi >= G * R) continue;
+    float M = -INFINITY;
+    for (int c = 0; c < a.n_chunks; ++c) M = fmaxf(M, a.part_ml[(zy * a.n_chunks + c) * 16 + q].x);
+    float L = 0.f, O = 0.f;
+    for (int c = 0; c < a.n_chunks; ++c) {
+      const float2 ml = a.part_ml[(zy * a.n_chunks + c) * 16 + q];
+      if (ml.x == -INFINITY) continue;
+      const float f = expf(ml.x - M);
+      L += ml.y * f;
+      O += a.part_o[((zy * a.n_chunks + c) * 16 + q) * HD + d] * f;
+    }
+    const int gh = qi / R, ri = qi % R;
+    const int m = win * R + ri;
+    const int head = kvh * G + gh;
+    pack_store(a.out, a.wtype, m, head * HD + d, O / L);
+  }
+}
+
+template <int KVB, int HD>
+hipError_t launch_hd(const AttnArgs& a, hipStream_t s) {
+  dim3 g1(a.n_chunks, a.n_qtiles, a.n_windows * a.n_kv);
+  hipLaunchKernelGGL((k_attn<KVB, HD>), g1, dim3(256), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  dim3 g2(a.n_qtiles, a.n_windows * a.n_kv);
+  hipLaunchKernelGGL((k_attn_combine<HD>), g2, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_attention(int kv_bf16, int hd, const AttnArgs& a, hipStream_t s) {
+  if (kv_bf16) {
+    switch (hd) {
+      case 32: return launch_hd<1, 32>(a, s);
+      case 64: return launch_hd<1, 64>(a, s);
+      case 96: return launch_hd<1, 96>(a, s);
+      case 128: return launch_hd<1, 128>(a, s);
+    }
+  } else {
+    switch (hd) {
+      case 32: return launch_hd<0, 32>(a, s);
+      case 64: return launch_hd<0, 64>(a, s);
+      case 96: return launch_hd<0, 96>(a, s);
+      case 128: return launch_hd<0, 128>(a, s);
+    }
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace dsi

@@ -1,0 +1,240 @@
+// Elementwise passes: weight pre-packing, embedding gather + RMSNorm into a
+// GEMM activation pack (plus the rotary cos/sin table of the window
+// positions), RMSNorm into a pack, and KV length / content operations.
+#include "device_util.h"
+
+namespace dsi {
+
+namespace {
+
+// deterministic block sum of one float per thread (blockDim.x = 256)
+__device__ float block_sum_256(float v, float* sh) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) sh[w] = v;
+  __syncthreads();
+  const float t = (sh[0] + sh[1]) + (sh[2] + sh[3]);
+  __syncthreads();
+  return t;
+}
+
+template <typename T>
+__global__ void k_prepack(const T* __restrict__ src, int N, int K, T* __restrict__ dst, int Kb,
+                          int dst_nb0, int n_blocks, int rowmap, int hd, int which) {
+  const size_t total = (size_t)n_blocks * Kb * 512;
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < total;
+       i += (size_t)gridDim.x * blockDim.x) {
+    const int e = (int)(i & 7);
+    const int lane = (int)((i >> 3) & 63);
+    const size_t tile = i >> 9;
+    const int kb = (int)(tile % Kb);
+    const int nbl = (int)(tile / Kb);       // section-local n-block
+    const int r = lane & 15, g = r >> 2, jj = r & 3;
+    const int k = kb * 32 + (lane >> 4) * 8 + e;
+    int row;
+    bool mine = true;
+    if (rowmap == 0) {
+      row = nbl * 16 + r;
+    } else if (rowmap == 1) {
+      const int bph = hd >> 4;
+      const int h = nbl / bph, j0 = (nbl % bph) * 8;
+      row = h * hd + j0 + 2 * g + (jj & 1) + (jj >> 1) * (hd >> 1);
+    } else {
+      mine = (jj >> 1) == which;
+      row = nbl * 8 + 2 * g + (jj & 1);
+    }
+    if (!mine) continue;
+    const T v = (row < N && k < K) ? src[(size_t)row * K + k] : T(0);
+    dst[(((size_t)(dst_nb0 + nbl) * Kb + kb) * 64 + lane) * 8 + e] = v;
+  }
+}
+
+__device__ __forceinline__ float load_w_elem(const void* p, int wtype, size_t i) {
+  return wtype == W_BF16 ? bf_bits2f(((const uint16_t*)p)[i]) : ((const float*)p)[i];
+}
+
+// one workgroup per token row
+__global__ __launch_bounds__(256) void k_embed_norm(EmbedArgs a) {
+  __shared__ float sh[4];
+  const int m = blockIdx.x;
+  int tok = a.tokens[m];
+  if (tok < 0 || tok >= a.V) {
+    if (threadIdx.x == 0) atomicOr(a.err, 1);
+    tok = 0;
+  }
+  float ss = 0.f;
+  for (int c = threadIdx.x; c < a.d; c += 256) {
+    const float v = load_w_elem(a.E, a.wtype, (size_t)tok * a.d + c);
+    a.x[(size_t)m * a.d + c] = v;
+    if (a.hidden0) a.hidden0[(size_t)m * a.d + c] = v;
+    ss += v * v;
+  }
+  const float tot = block_sum_256(ss, sh);
+  const float rs = 1.0f / sqrtf(tot / (float)a.d + a.eps);
+  for (int c = threadIdx.x; c < a.d; c += 256) {
+    const float v = load_w_elem(a.E, a.wtype, (size_t)tok * a.d + c);
+    pack_store(a.pack, a.wtype, m, c, v * rs * a.gain[c]);
+  }
+  // rotary table of this row's position: angle = pos * base^(-2j/hd), fp64
+  const int R = a.rows.rows_per_window;
+  const int pos = a.rows.lens[a.rows.window0 + m / R] + (m % R);
+  const int half = a.hd >> 1;
+  for (int j = threadIdx.x; j < half; j += 256) {
+    const double inv = exp2(-2.0 * (double)j / (double)a.hd * a.log2_base);
+    double s, c;
+    sincos((double)pos * inv, &s, &c);
+    a.rope[(size_t)m * half + j] = make_float2((float)c, (float)s);
+  }
+}
+
+__global__ __launch_bounds__(256) void k_rmsnorm_pack(const float* __restrict__ x, int d,
+                                                       const float* __restrict__ gain, float eps,
+                                                       int wtype, PackRef pack, float* copy_out) {
+  __shared__ float sh[4];
+  const int m = blockIdx.x;
+  const float* xr = x + (size_t)m * d;
+  float ss = 0.f;
+  for (int c = threadIdx.x; c < d; c += 256) {
+    const float v = xr[c];
+    ss += v * v;
+    if (copy_out) copy_out[(size_t)m * d + c] = v;
+  }
+  const float tot = block_sum_256(ss, sh);
+  const float rs = 1.0f / sqrtf(tot / (float)d + eps);
+  for (int c = threadIdx.x; c < d; c += 256) pack_store(pack, wtype, m, c, xr[c] * rs * gain[c]);
+}
+
+__global__ void k_kv_rollback(int* lens, int window, int new_len, int* err) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) {
+    if (new_len < 0 || new_len > lens[window]) atomicOr(err, 4);
+    else lens[window] = new_len;
+  }
+}
+__global__ void k_kv_set(int* lens, int window, int v) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) lens[window] = v;
+}
+// advance a window by n prompt tokens if every id is valid
+__global__ void k_kv_add_checked(int* lens, int window, const int* tokens, int n, int V, int* err) {
+  __shared__ int bad;
+  if (threadIdx.x == 0) bad = 0;
+  __syncthreads();
+  for (int i = threadIdx.x; i < n; i += blockDim.x)
+    if (tokens[i] < 0 || tokens[i] >= V) bad = 1;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    if (bad) atomicOr(err, 1);
+    else lens[window] += n;
+  }
+}
+
+// copy [n_kv][len][hd] <-> cache (K [n_kv][maxlen][hd], V^T [n_kv][hd][maxlen])
+template <typename T>
+__global__ void k_kv_copy(int to_cache, T* kc, T* vc, int n_kv, int hd, int maxlen, int len,
+                          T* dk, T* dv) {
+  const size_t total = (size_t)n_kv * len * hd;
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < total;
+       i += (size_t)gridDim.x * blockDim.x) {
+    const int dd = (int)(i % hd);
+    const int p = (int)((i / hd) % len);
+    const int h = (int)(i / ((size_t)hd * len));
+    const size_t ki = ((size_t)h * maxlen + p) * hd + dd;
+    const size_t vi = ((size_t)h * hd + dd) * maxlen + p;
+    if (to_cache) {
+      kc[ki] = dk[i];
+      vc[vi] = dv[i];
+    } else {
+      dk[i] = kc[ki];
+      dv[i] = vc[vi];
+    }
+  }
+}
+
+__global__ void k_fill_zero(uint32_t* p, size_t n) {
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    p[i] = 0u;
+}
+
+__global__ void k_copy(const float* __restrict__ s, float* __restrict__ d, size_t n) {
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    d[i] = s[i];
+}
+
+int grid_for(size_t n, int block) {
+  size_t g = (n + block - 1) / block;
+  if (g > 65536) g = 65536;
+  if (g < 1) g = 1;
+  return (int)g;
+}
+
+}  // namespace
+
+hipError_t launch_prepack(int wtype, const void* src, int N, int K, void* dst, int Kb, int dst_nb0,
+                          int rowmap, int hd, int which, hipStream_t s) {
+  int n_blocks;
+  if (rowmap == 2) n_blocks = (N + 7) / 8;
+  else n_blocks = (N + 15) / 16;
+  const size_t total = (size_t)n_blocks * Kb * 512;
+  const int g = grid_for(total, 256);
+  if (wtype == W_BF16)
+    hipLaunchKernelGGL(k_prepack<uint16_t>, dim3(g), dim3(256), 0, s, (const uint16_t*)src, N, K,
+                       (uint16_t*)dst, Kb, dst_nb0, n_blocks, rowmap, hd, which);
+  else
+    hipLaunchKernelGGL(k_prepack<float>, dim3(g), dim3(256), 0, s, (const float*)src, N, K,
+                       (float*)dst, Kb, dst_nb0, n_blocks, rowmap, hd, which);
+  return hipGetLastError();
+}
+
+hipError_t launch_embed_norm(const EmbedArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(k_embed_norm, dim3(a.M), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm_pack(const float* x, int M, int d, const float* gain, float eps, int wtype,
+                               PackRef pack, float* copy_out, hipStream_t s) {
+  hipLaunchKernelGGL(k_rmsnorm_pack, dim3(M), dim3(256), 0, s, x, d, gain, eps, wtype, pack, copy_out);
+  return hipGetLastError();
+}
+
+hipError_t launch_kv_rollback(int* lens, int window, int new_len, int* err, hipStream_t s) {
+  hipLaunchKernelGGL(k_kv_rollback, dim3(1), dim3(64), 0, s, lens, window, new_len, err);
+  return hipGetLastError();
+}
+hipError_t launch_kv_set(int* lens, int window, int new_len, hipStream_t s) {
+  hipLaunchKernelGGL(k_kv_set, dim3(1), dim3(64), 0, s, lens, window, new_len);
+  return hipGetLastError();
+}
+hipError_t launch_kv_add_checked(int* lens, int window, const int* tokens, int n, int V, int* err,
+                                 hipStream_t s) {
+  hipLaunchKernelGGL(k_kv_add_checked, dim3(1), dim3(256), 0, s, lens, window, tokens, n, V, err);
+  return hipGetLastError();
+}
+
+hipError_t launch_kv_copy(int to_cache, int kv_bf16, void* kc, void* vc, int n_kv, int hd, int maxlen,
+                          int len, void* dk, void* dv, hipStream_t s) {
+  const size_t total = (size_t)n_kv * len * hd;
+  if (total == 0) return hipSuccess;
+  const int g = grid_for(total, 256);
+  if (kv_bf16)
+    hipLaunchKernelGGL(k_kv_copy<uint16_t>, dim3(g), dim3(256), 0, s, to_cache, (uint16_t*)kc,
+                       (uint16_t*)vc, n_kv, hd, maxlen, len, (uint16_t*)dk, (uint16_t*)dv);
+  else
+    hipLaunchKernelGGL(k_kv_copy<float>, dim3(g), dim3(256), 0, s, to_cache, (float*)kc, (float*)vc,
+                       n_kv, hd, maxlen, len, (float*)dk, (float*)dv);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s) {
+  const size_t n = bytes / 4;
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_fill_zero, dim3(grid_for(n, 256)), dim3(256), 0, s, (uint32_t*)p, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_rows(const float* src, float* dst, size_t n, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_copy, dim3(grid_for(n, 256)), dim3(256), 0, s, src, dst, n);
+  return hipGetLastError();
+}
+
+}  // namespace dsi

@@ -1,0 +1,278 @@
+// Window GEMM: Y[M, N] = X[M, K] . W[N, K]^T for the k+1 (or a few dozen)
+// rows of a verification window, with fused epilogues.
+//
+// The k+1 window rows are one batch through the target (Section 2): every
+// weight byte is read once per verification while each weight feeds only M
+// (6..64) rows, so the kernel is bound by streaming W from HBM.  Design:
+//  * W is pre-packed into 1 KB MFMA tiles (16 rows x 32 k, bf16), one
+//    dwordx4 per lane, so every wavefront load is 1 KB contiguous and lands
+//    in registers already in A-operand order (no LDS round trip for W);
+//  * activations come as pre-split bf16 hi/lo packs (B operand, L2-resident)
+//    and each tile costs two 16x16x32 MFMAs, giving ~fp32 accuracy;
+//  * a workgroup owns NBW n-blocks (16 features each) and its NW waves split
+//    K; partial tiles are reduced through LDS in a fixed order
+//    (deterministic, no float atomics) and handed to the epilogue;
+//  * weight loads for the next U k-blocks are issued before the MFMAs of the
+//    current ones so every wave keeps U*NBW KB in flight.
+#include "device_util.h"
+
+namespace dsi {
+
+namespace {
+
+template <int WT>
+__device__ __forceinline__ void epilogue(const EpiArgs& e, int nb, int r0, int m, f32x4 s) {
+  switch (e.kind) {
+    case EPI_STORE: {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int n = nb * 16 + r0 + j;
+        if (n < e.n_valid) e.out[(size_t)m * e.ld + n] = s[j];
+      }
+      break;
+    }
+    case EPI_RESID: {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int n = nb * 16 + r0 + j;
+        if (n < e.n_valid) e.out[(size_t)m * e.ld + n] += s[j];
+      }
+      break;
+    }
+    case EPI_SILU: {
+      // rows 4g+0, 4g+1: gate of features f, f+1; rows 4g+2, 4g+3: up
+      const int f = nb * 8 + (r0 >> 2) * 2;
+      if (f < e.ff) pack_store(e.pack, WT, m, f, silu_f(s[0]) * s[2]);
+      if (f + 1 < e.ff) pack_store(e.pack, WT, m, f + 1, silu_f(s[1]) * s[3]);
+      break;
+    }
+    case EPI_QKV: {
+      const int hd = e.hd;
+      const int bph = hd >> 4;                       // 16-row blocks per head
+      const int nq = e.n_heads * bph, nk = e.n_kv * bph;
+      const int R = e.rows.rows_per_window;
+      const int win = e.rows.window0 + m / R;
+      const int pos = e.rows.lens[win] + (m % R);
+      if (nb < nq + nk) {
+        const int sb = nb < nq ? nb : nb - nq;
+        const int h = sb / bph;
+        const int ja = (sb % bph) * 8 + (r0 >> 2) * 2;   // pair indices ja, ja+1
+        const int half = hd >> 1;
+        const float2 ca = e.rope[(size_t)m * half + ja];
+        const float2 cb = e.rope[(size_t)m * half + ja + 1];
+        const float a1 = s[0] * ca.x - s[2] * ca.y, a2 = s[2] * ca.x + s[0] * ca.y;
+        const float b1 = s[1] * cb.x - s[3] * cb.y, b2 = s[3] * cb.x + s[1] * cb.y;
+        if (nb < nq) {
+          float* qr = e.q_out + (size_t)m * (e.n_heads * hd) + h * hd;
+          qr[ja] = a1;
+          qr[ja + half] = a2;
+          qr[ja + 1] = b1;
+          qr[ja + 1 + half] = b2;
+        } else {
+          const size_t base = (((size_t)win * e.n_kv + h) * e.maxlen + pos) * hd;
+          if (e.kv_bf16) {
+            uint16_t* kc = (uint16_t*)e.kcache + base;
+            kc[ja] = f2bf_bits(a1);
+            kc[ja + half] = f2bf_bits(a2);
+            kc[ja + 1] = f2bf_bits(b1);
+            kc[ja + 1 + half] = f2bf_bits(b2);
+          } else {
+            float* kc = (float*)e.kcache + base;
+            kc[ja] = a1;
+            kc[ja + half] = a2;
+            kc[ja + 1] = b1;
+            kc[ja + 1 + half] = b2;
+          }
+        }
+      } else {
+        const int vb = nb - nq - nk;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int n = vb * 16 + r0 + j;
+          const int h = n / hd, dd = n % hd;
+          const size_t idx = (((size_t)win * e.n_kv + h) * hd + dd) * e.maxlen + pos;
+          if (e.kv_bf16) ((uint16_t*)e.vcache)[idx] = f2bf_bits(s[j]);
+          else ((float*)e.vcache)[idx] = s[j];
+        }
+      }
+      break;
+    }
+  }
+}
+
+template <int MT, int NBW, int NW, int U>
+__global__ __launch_bounds__(NW * 64) void k_gemm_bf16(GemmArgs a) {
+  constexpr int ACC = NBW * MT;
+  __shared__ f32x4 red[NW * ACC * 64];
+  const int lane = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+  const int nb0 = blockIdx.x * NBW;
+  const int nbv = min(NBW, a.Nb - nb0);
+  const int per = (a.Kb + NW - 1) / NW;
+  const int kb_beg = min(a.Kb, w * per);
+  const int kb_end = min(a.Kb, kb_beg + per);
+  const u32x4* __restrict__ W = (const u32x4*)a.W;
+  const u32x4* __restrict__ Xh = (const u32x4*)a.Xhi;
+  const u32x4* __restrict__ Xl = (const u32x4*)a.Xlo;
+
+  f32x4 acc[NBW][MT];
+#pragma unroll
+  for (int j = 0; j < NBW; ++j)
+#pragma unroll
+    for (int t = 0; t < MT; ++t) acc[j][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  u32x4 cur[U][NBW];
+  auto load_w = [&](u32x4 (&dst)[U][NBW], int kb) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int j = 0; j < NBW; ++j) {
+        if (kb + u < kb_end && j < nbv)
+          dst[u][j] = __builtin_nontemporal_load(&W[((size_t)(nb0 + j) * a.Kb + kb + u) * 64 + lane]);
+        else
+          dst[u][j] = u32x4{0u, 0u, 0u, 0u};
+      }
+  };
+  if (kb_beg < kb_end) load_w(cur, kb_beg);
+  for (int kb = kb_beg; kb < kb_end; kb += U) {
+    u32x4 nxt[U][NBW];
+    if (kb + U < kb_end) load_w(nxt, kb + U);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (kb + u < kb_end) {
+#pragma unroll
+        for (int t = 0; t < MT; ++t) {
+          const size_t xi = ((size_t)t * a.Kb + kb + u) * 64 + lane;
+          const bf16x8 xh = as_bf16x8(Xh[xi]);
+          const bf16x8 xl = as_bf16x8(Xl[xi]);
+#pragma unroll
+          for (int j = 0; j < NBW; ++j) {
+            const bf16x8 wv = as_bf16x8(cur[u][j]);
+            acc[j][t] = mfma_bf16(wv, xh, acc[j][t]);
+            acc[j][t] = mfma_bf16(wv, xl, acc[j][t]);
+          }
+        }
+      }
+    }
+    if (kb + U < kb_end) {
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int j = 0; j < NBW; ++j) cur[u][j] = nxt[u][j];
+    }
+  }
+
+#pragma unroll
+  for (int j = 0; j < NBW; ++j)
+#pragma unroll
+    for (int t = 0; t < MT; ++t) red[((w * NBW + j) * MT + t) * 64 + lane] = acc[j][t];
+  __syncthreads();
+  for (int it = threadIdx.x; it < ACC * 64; it += NW * 64) {
+    const int l = it & 63, jm = it >> 6;
+    const int j = jm / MT, t = jm % MT;
+    f32x4 s = red[jm * 64 + l];
+    for (int ww = 1; ww < NW; ++ww) s += red[(ww * ACC + jm) * 64 + l];
+    const int nb = nb0 + j, m = t * 16 + (l & 15);
+    if (nb < a.Nb && m < a.M) epilogue<W_BF16>(a.epi, nb, (l >> 4) * 4, m, s);
+  }
+}
+
+template <int MT, int NBW, int NW>
+__global__ __launch_bounds__(NW * 64) void k_gemm_f32(GemmArgs a) {
+  constexpr int ACC = NBW * MT;
+  __shared__ f32x4 red[NW * ACC * 64];
+  const int lane = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+  const int nb0 = blockIdx.x * NBW;
+  const int nbv = min(NBW, a.Nb - nb0);
+  const int per = (a.Kb + NW - 1) / NW;
+  const int kb_beg = min(a.Kb, w * per);
+  const int kb_end = min(a.Kb, kb_beg + per);
+  const float4* __restrict__ W = (const float4*)a.W;
+  const float4* __restrict__ X = (const float4*)a.Xhi;
+
+  f32x4 acc[NBW][MT];
+#pragma unroll
+  for (int j = 0; j < NBW; ++j)
+#pragma unroll
+    for (int t = 0; t < MT; ++t) acc[j][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int kb = kb_beg; kb < kb_end; ++kb) {
+    F8 wf[NBW];
+#pragma unroll
+    for (int j = 0; j < NBW; ++j) {
+      if (j < nbv) {
+        const size_t wi = (((size_t)(nb0 + j) * a.Kb + kb) * 64 + lane) * 2;
+        wf[j].a = W[wi];
+        wf[j].b = W[wi + 1];
+      } else {
+        wf[j].a = wf[j].b = float4{0.f, 0.f, 0.f, 0.f};
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < MT; ++t) {
+      const size_t xi = (((size_t)t * a.Kb + kb) * 64 + lane) * 2;
+      F8 xf;
+      xf.a = X[xi];
+      xf.b = X[xi + 1];
+#pragma unroll
+      for (int e8 = 0; e8 < 8; ++e8)
+#pragma unroll
+        for (int j = 0; j < NBW; ++j) acc[j][t] = mfma_f32(f8_get(wf[j], e8), f8_get(xf, e8), acc[j][t]);
+    }
+  }
+
+#pragma unroll
+  for (int j = 0; j < NBW; ++j)
+#pragma unroll
+    for (int t = 0; t < MT; ++t) red[((w * NBW + j) * MT + t) * 64 + lane] = acc[j][t];
+  __syncthreads();
+  for (int it = threadIdx.x; it < ACC * 64; it += NW * 64) {
+    const int l = it & 63, jm = it >> 6;
+    const int j = jm / MT, t = jm % MT;
+    f32x4 s = red[jm * 64 + l];
+    for (int ww = 1; ww < NW; ++ww) s += red[(ww * ACC + jm) * 64 + l];
+    const int nb = nb0 + j, m = t * 16 + (l & 15);
+    if (nb < a.Nb && m < a.M) epilogue<W_F32>(a.epi, nb, (l >> 4) * 4, m, s);
+  }
+}
+
+template <int MT>
+hipError_t launch_bf16(const GemmArgs& a, hipStream_t s) {
+  constexpr int NBW = 2, NW = 8, U = 4;
+  const int grid = (a.Nb + NBW - 1) / NBW;
+  hipLaunchKernelGGL((k_gemm_bf16<MT, NBW, NW, U>), dim3(grid), dim3(NW * 64), 0, s, a);
+  return hipGetLastError();
+}
+
+template <int MT>
+hipError_t launch_f32(const GemmArgs& a, hipStream_t s) {
+  constexpr int NBW = 1, NW = 4;
+  const int grid = (a.Nb + NBW - 1) / NBW;
+  hipLaunchKernelGGL((k_gemm_f32<MT, NBW, NW>), dim3(grid), dim3(NW * 64), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_gemm(int wtype, int mt, const GemmArgs& a, hipStream_t s) {
+  if (a.Nb <= 0 || a.M <= 0) return hipSuccess;
+  if (wtype == W_BF16) {
+    switch (mt) {
+      case 1: return launch_bf16<1>(a, s);
+      case 2: return launch_bf16<2>(a, s);
+      case 3: return launch_bf16<3>(a, s);
+      case 4: return launch_bf16<4>(a, s);
+    }
+  } else {
+    switch (mt) {
+      case 1: return launch_f32<1>(a, s);
+      case 2: return launch_f32<2>(a, s);
+      case 3: return launch_f32<3>(a, s);
+      case 4: return launch_f32<4>(a, s);
+    }
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace dsi

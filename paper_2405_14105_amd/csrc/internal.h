@@ -1,0 +1,177 @@
+// Internal declarations shared by the kernel translation units and the
+// runtime.  gfx950 (CDNA4) only: 64-wide wavefronts, bf16/fp32 MFMA.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace dsi {
+
+// ----------------------------------------------------------------- layouts
+//
+// Streaming tile ("packed") layout of a GEMM weight W [N, K] (rows = output
+// features): tiles of 16 rows x 32 k, stored [Nb][Kb][64 lanes][8 elems] so
+// that one wavefront loads one tile as 64 x 16 B (bf16) contiguous bytes --
+// exactly the A-operand fragment of a 16x16x32 MFMA: lane l holds row
+// (l % 16) and k = 8 * (l / 16) + e, e = 0..7.  Rows and k beyond N, K are 0.
+//
+// Activation pack for a GEMM input X [M, K]: [Mt][Kb][64][8] with lane l
+// holding token (l % 16) and the same k mapping -- the B-operand fragment.
+// For bf16 weights an fp32 activation x is carried as two bf16 packs,
+// hi = bf16(x) and lo = bf16(x - hi), and each tile costs two MFMAs, so the
+// GEMM is accurate to ~2^-17 relative instead of bf16's 2^-9.  For fp32
+// weights the pack holds fp32 and the fp32 MFMA 16x16x4 is used.
+//
+// MFMA output (16x16, fp32): lane l holds rows 4*(l/16) + j, j = 0..3, of
+// column l % 16 -- four output features of one token.
+//
+// Row order inside a 16-row tile for two fused epilogues:
+//  * RoPE pairing (Q and K sections of the fused QKV weight): tile row
+//    4g + jj holds pair index 2g + (jj & 1) and half (jj >> 1), so a lane
+//    owns both members (x_j, x_{j+hd/2}) of two rotary pairs.
+//  * SwiGLU interleave (fused gate/up weight): tile row 4g + jj holds FFN
+//    feature 8*nb + 2g + (jj & 1), gate for jj < 2 and up for jj >= 2.
+//
+// KV cache of one layer and window: K [n_kv][max_len_pad][hd] and the value
+// cache transposed, V^T [n_kv][hd][max_len_pad], so that both attention
+// MFMAs read 16 contiguous bytes per lane.
+
+enum WType : int { W_F32 = 0, W_BF16 = 1 };
+
+constexpr int kTileRows = 16;
+constexpr int kTileK = 32;
+constexpr int kMaxMt = 4;          // at most 64 rows per forward chunk
+constexpr int kMaxRows = kMaxMt * 16;
+
+// gemm epilogues
+enum Epi : int { EPI_STORE = 0, EPI_RESID = 1, EPI_QKV = 2, EPI_SILU = 3 };
+
+struct PackRef {        // an activation pack (hi/lo bf16, or fp32 in hi)
+  void* hi;
+  void* lo;
+  int Kb;               // k-blocks of the consuming GEMM
+};
+
+struct RowMap {         // token row m -> (window, row within window, position)
+  const int* lens;      // device window lengths
+  int window0;
+  int rows_per_window;  // R
+};
+
+struct EpiArgs {
+  int kind;
+  // EPI_STORE: out [M][ld]; EPI_RESID: x [M][ld] += acc
+  float* out;
+  int ld;
+  int n_valid;          // logical N (features) -- outputs beyond are dropped
+  // EPI_QKV
+  float* q_out;         // [M][n_heads*hd]
+  void* kcache;         // layer base: [windows][n_kv][maxlen][hd]
+  void* vcache;         // layer base: [windows][n_kv][hd][maxlen]
+  int kv_bf16;
+  int n_heads, n_kv, hd, maxlen;
+  const float2* rope;   // [M][hd/2] (cos, sin)
+  RowMap rows;
+  // EPI_SILU
+  PackRef pack;
+  int ff;
+};
+
+struct GemmArgs {
+  const void* W;
+  const void* Xhi;
+  const void* Xlo;
+  int Nb, Kb, M;
+  EpiArgs epi;
+};
+
+// launchers (gemm.hip)
+hipError_t launch_gemm(int wtype, int mt, const GemmArgs& a, hipStream_t s);
+
+// prepack (elementwise.hip): src [N][K] row-major (device), dst packed.
+// rowmap: 0 plain, 1 rope-paired (QKV sections), 2 gate/up interleave
+// (which = 0 gate, 1 up).  dst_nb0: first destination n-block.
+hipError_t launch_prepack(int wtype, const void* src, int N, int K, void* dst, int Kb,
+                          int dst_nb0, int rowmap, int hd, int which, hipStream_t s);
+
+// embed gather + RMSNorm + pack + rope table (elementwise.hip)
+struct EmbedArgs {
+  const int* tokens;    // [M]
+  const void* E;        // [V][d] wdtype
+  int wtype;
+  int V, d, M;
+  float* x;             // [M][d] residual out
+  const float* gain;    // first layer attention-norm gain
+  float eps;
+  PackRef pack;
+  float2* rope;         // [M][hd/2]
+  int hd;
+  double log2_base;
+  RowMap rows;
+  int* err;
+  float* hidden0;       // optional copy of x (diagnostics)
+};
+hipError_t launch_embed_norm(const EmbedArgs& a, hipStream_t s);
+
+// RMSNorm of x rows into a pack; also optional diagnostic copy of x
+hipError_t launch_rmsnorm_pack(const float* x, int M, int d, const float* gain, float eps,
+                               int wtype, PackRef pack, float* copy_out, hipStream_t s);
+
+// attention (attention.hip)
+struct AttnArgs {
+  const float* q;       // [M][n_heads*hd]
+  const void* kc;       // layer base
+  const void* vc;
+  RowMap rows;
+  int n_windows;
+  int n_heads, n_kv, maxlen;
+  int n_qtiles, chunk, n_chunks;
+  float scale;
+  float* part_o;        // [windows*n_kv][qtiles][chunks][16][hd]
+  float2* part_ml;      // [windows*n_kv][qtiles][chunks][16]
+  PackRef out;          // O-projection input pack
+  int wtype;
+};
+hipError_t launch_attention(int kv_bf16, int hd, const AttnArgs& a, hipStream_t s);
+
+// verification (verify.hip)
+struct VerifyArgs {
+  int B, k, V;
+  const float* logits;  // [B*(k+1)][V]
+  const int* tokens;    // [B][k+1]
+  const float* q;       // [B][k][V]
+  const float* u;       // [B][k+1]
+  double temperature;
+  int greedy;
+  int commit;
+  int* lens;            // nullable: window lengths (commit)
+  int window0;
+  int* n_out;
+  int* tok_out;
+  int* err;
+  // workspace
+  double2* part;        // [B*(k+1)][C]: (max, sumexp)
+  float2* part_arg;     // [B*(k+1)][C]: (max value, index as float bits)
+  double2* rowstat;     // [B*(k+1)]: (M, S)
+  int* rowarg;          // [B*(k+1)]
+  int4* decision;       // [B]: (n, row, residual, err)
+  double2* csum;        // [B][C]: (sum r, sum p)
+  int C;                // chunks per row
+};
+constexpr int kVerifyChunk = 4096;  // vocabulary entries per chunk (256 thr x 16)
+size_t verify_workspace_bytes(int rows, int B, int V);
+void verify_bind_workspace(VerifyArgs& a, void* ws, int rows, int B, int V);
+hipError_t launch_verify(const VerifyArgs& a, hipStream_t s);
+
+// KV and misc (elementwise.hip)
+hipError_t launch_kv_rollback(int* lens, int window, int new_len, int* err, hipStream_t s);
+hipError_t launch_kv_set(int* lens, int window, int new_len, hipStream_t s);
+hipError_t launch_kv_add_checked(int* lens, int window, const int* tokens, int n, int V, int* err,
+                                 hipStream_t s);
+hipError_t launch_kv_copy(int to_cache, int kv_bf16, void* kc, void* vc, int n_kv, int hd,
+                          int maxlen, int len, void* dk, void* dv, hipStream_t s);
+hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
+hipError_t launch_copy_rows(const float* src, float* dst, size_t n, hipStream_t s);
+
+}  // namespace dsi

@@ -1,0 +1,736 @@
+// Host runtime behind the C ABI: model and KV-cache objects, the launch plan
+// of one target forward over a batch of window rows, and the verification /
+// prefill / rollback entry points.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <map>
+#include <mutex>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/dsi.h"
+#include "internal.h"
+
+using namespace dsi;
+
+namespace {
+
+thread_local std::string g_err;
+
+dsi_status fail(dsi_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+#define HIP_TRY(expr)                                                              \
+  do {                                                                             \
+    hipError_t e_ = (expr);                                                        \
+    if (e_ != hipSuccess)                                                          \
+      return fail(DSI_EHIP, "%s failed: %s", #expr, hipGetErrorString(e_));        \
+  } while (0)
+
+#define DSI_TRY(expr)               \
+  do {                              \
+    dsi_status s_ = (expr);         \
+    if (s_ != DSI_OK) return s_;    \
+  } while (0)
+
+size_t round_up(size_t x, size_t m) { return (x + m - 1) / m * m; }
+int cdiv(int a, int b) { return (a + b - 1) / b; }
+
+struct DevBuf {
+  void* p = nullptr;
+  size_t bytes = 0;
+};
+
+dsi_status ensure(DevBuf& b, size_t bytes) {
+  if (b.bytes >= bytes) return DSI_OK;
+  if (b.p) {
+    hipError_t e = hipFree(b.p);
+    b.p = nullptr;
+    b.bytes = 0;
+    if (e != hipSuccess) return fail(DSI_EHIP, "hipFree: %s", hipGetErrorString(e));
+  }
+  hipError_t e = hipMalloc(&b.p, bytes);
+  if (e != hipSuccess) {
+    hipGetLastError();
+    b.p = nullptr;
+    return fail(DSI_ENOMEM, "hipMalloc(%zu) failed: %s", bytes, hipGetErrorString(e));
+  }
+  b.bytes = bytes;
+  return DSI_OK;
+}
+
+}  // namespace
+
+struct LayerW {
+  float* attn_norm = nullptr;
+  float* ffn_norm = nullptr;
+  void* wqkv = nullptr;
+  void* wo = nullptr;
+  void* wgu = nullptr;
+  void* wdown = nullptr;
+};
+
+struct dsi_model {
+  dsi_config cfg;
+  hipStream_t stream = nullptr;
+  int wtype = 0, kvb = 0, esz = 4, kvesz = 4;
+  int d = 0, hq = 0, hkv = 0, hd = 0, qdim = 0, kvdim = 0, ff = 0, V = 0, L = 0;
+  int Kb_d = 0, Kb_q = 0, Kb_ff = 0;
+  int Nb_qkv = 0, Nb_o = 0, Nb_gu = 0, Nb_down = 0, Nb_head = 0;
+  void* embed = nullptr;
+  float* final_norm = nullptr;
+  void* lm_head = nullptr;
+  std::vector<LayerW> layers;
+  std::vector<unsigned> set_mask;   // [L+1]: bit per tensor id (index 0: globals)
+  std::vector<void*> allocs;
+  // forward workspace for up to kMaxRows rows
+  float* x = nullptr;
+  PackRef pk_d{}, pk_q{}, pk_ff{};
+  float* qbuf = nullptr;
+  float2* rope = nullptr;
+  float* logits = nullptr;
+  void* vws = nullptr;
+  int* err = nullptr;
+  DevBuf attn_o, attn_ml;
+  int live_kv = 0;
+};
+
+struct dsi_kv {
+  dsi_model* m = nullptr;
+  int n_windows = 0, max_len = 0, maxlen_pad = 0;
+  void* k = nullptr;
+  void* v = nullptr;
+  int* lens = nullptr;
+  std::vector<long long> hi, lo;   // host bounds on each window's length
+  size_t win_elems = 0;            // elements of one (layer, window) of K (= of V)
+};
+
+namespace {
+
+dsi_status dev_alloc(std::vector<void*>& list, void** p, size_t bytes) {
+  if (bytes == 0) bytes = 16;
+  hipError_t e = hipMalloc(p, bytes);
+  if (e != hipSuccess) {
+    hipGetLastError();
+    *p = nullptr;
+    return fail(DSI_ENOMEM, "hipMalloc(%zu) failed: %s", bytes, hipGetErrorString(e));
+  }
+  list.push_back(*p);
+  e = hipMemset(*p, 0, bytes);
+  if (e != hipSuccess) return fail(DSI_EHIP, "hipMemset failed: %s", hipGetErrorString(e));
+  return DSI_OK;
+}
+
+void free_list(std::vector<void*>& list) {
+  for (void* p : list) hipFree(p);
+  list.clear();
+}
+
+bool all_set(const dsi_model* m) {
+  const unsigned glob = (1u << DSI_T_EMBED) | (1u << DSI_T_FINAL_NORM) | (1u << DSI_T_LM_HEAD);
+  const unsigned lay = 0xFF8u;   // ids 3..11
+  if ((m->set_mask[0] & glob) != glob) return false;
+  for (int l = 0; l < m->L; ++l)
+    if ((m->set_mask[l + 1] & lay) != lay) return false;
+  return true;
+}
+
+void* kv_ptr(const dsi_kv* kv, void* base, int layer, int window) {
+  const size_t off = ((size_t)layer * kv->n_windows + window) * kv->win_elems;
+  return (char*)base + off * kv->m->kvesz;
+}
+
+PackRef make_pack(dsi_model* m, int Kb, dsi_status* st) {
+  PackRef p{};
+  p.Kb = Kb;
+  const size_t elems = (size_t)kMaxMt * Kb * 512;
+  *st = dev_alloc(m->allocs, &p.hi, elems * m->esz);
+  if (*st == DSI_OK && m->wtype == W_BF16) *st = dev_alloc(m->allocs, &p.lo, elems * 2);
+  return p;
+}
+
+// ------------------------------------------------------------- forward plan
+//
+// One target forward over M = B * R rows: R consecutive rows of each of the
+// B windows window0..window0+B-1, appended after each window's cached
+// length.  Writes the rows' K/V into the cache (the window length itself is
+// advanced by the caller).  logits: nullptr (no head), else [M][V]
+// (head_last_only: only the last row, into logits[0..V)).
+dsi_status run_forward(dsi_model* m, dsi_kv* kv, int window0, int B, int R, const int* d_tokens,
+                       float* logits, int head_last_only, float* hidden) {
+  hipStream_t s = m->stream;
+  const int M = B * R;
+  const int mt = cdiv(M, 16);
+  RowMap rows{kv->lens, window0, R};
+  const size_t Md = (size_t)M * m->d;
+
+  EmbedArgs ea{};
+  ea.tokens = d_tokens;
+  ea.E = m->embed;
+  ea.wtype = m->wtype;
+  ea.V = m->V;
+  ea.d = m->d;
+  ea.M = M;
+  ea.x = m->x;
+  ea.gain = m->layers[0].attn_norm;
+  ea.eps = m->cfg.rms_eps;
+  ea.pack = m->pk_d;
+  ea.rope = m->rope;
+  ea.hd = m->hd;
+  ea.log2_base = log2((double)m->cfg.rope_base);
+  ea.rows = rows;
+  ea.err = m->err;
+  ea.hidden0 = hidden;
+  HIP_TRY(launch_embed_norm(ea, s));
+
+  // attention split over key chunks, sized from the host bound on lengths
+  long long kmax = 0;
+  for (int b = 0; b < B; ++b) kmax = std::max(kmax, kv->hi[window0 + b] + R);
+  // The chunk size depends only on the model, R and the cache capacity --
+  // never on B or the current lengths -- so a window's partial sums and
+  // therefore its results are identical alone or inside a batch.
+  const int G = m->hq / m->hkv;
+  const int n_qtiles = cdiv(G * R, 16);
+  const int zq = B * m->hkv * n_qtiles;
+  const int want = std::max(1, cdiv(1024, m->hkv * n_qtiles));
+  int chunk = (int)round_up((size_t)cdiv(kv->max_len, want), 128);
+  chunk = std::min(std::max(chunk, 128), 8192);
+  const int n_chunks = (int)((kmax + chunk - 1) / chunk);
+  const size_t nparts = (size_t)zq * n_chunks * 16;
+  DSI_TRY(ensure(m->attn_o, nparts * m->hd * sizeof(float)));
+  DSI_TRY(ensure(m->attn_ml, nparts * sizeof(float2)));
+
+  for (int l = 0; l < m->L; ++l) {
+    const LayerW& lw = m->layers[l];
+    GemmArgs g{};
+    g.M = M;
+    // fused QKV + RoPE + KV append
+    g.W = lw.wqkv;
+    g.Xhi = m->pk_d.hi;
+    g.Xlo = m->pk_d.lo;
+    g.Nb = m->Nb_qkv;
+    g.Kb = m->Kb_d;
+    g.epi.kind = EPI_QKV;
+    g.epi.q_out = m->qbuf;
+    g.epi.kcache = kv_ptr(kv, kv->k, l, 0);
+    g.epi.vcache = kv_ptr(kv, kv->v, l, 0);
+    g.epi.kv_bf16 = m->kvb;
+    g.epi.n_heads = m->hq;
+    g.epi.n_kv = m->hkv;
+    g.epi.hd = m->hd;
+    g.epi.maxlen = kv->maxlen_pad;
+    g.epi.rope = m->rope;
+    g.epi.rows = rows;
+    HIP_TRY(launch_gemm(m->wtype, mt, g, s));
+
+    AttnArgs aa{};
+    aa.q = m->qbuf;
+    aa.kc = kv_ptr(kv, kv->k, l, 0);
+    aa.vc = kv_ptr(kv, kv->v, l, 0);
+    aa.rows = rows;
+    aa.n_windows = B;
+    aa.n_heads = m->hq;
+    aa.n_kv = m->hkv;
+    aa.maxlen = kv->maxlen_pad;
+    aa.n_qtiles = n_qtiles;
+    aa.chunk = chunk;
+    aa.n_chunks = n_chunks;
+    aa.scale = (float)(1.0 / sqrt((double)m->hd));
+    aa.part_o = (float*)m->attn_o.p;
+    aa.part_ml = (float2*)m->attn_ml.p;
+    aa.out = m->pk_q;
+    aa.wtype = m->wtype;
+    // windows beyond window0 are addressed through rows.window0 + win
+    HIP_TRY(launch_attention(m->kvb, m->hd, aa, s));
+
+    // O projection + residual
+    GemmArgs go{};
+    go.M = M;
+    go.W = lw.wo;
+    go.Xhi = m->pk_q.hi;
+    go.Xlo = m->pk_q.lo;
+    go.Nb = m->Nb_o;
+    go.Kb = m->Kb_q;
+    go.epi.kind = EPI_RESID;
+    go.epi.out = m->x;
+    go.epi.ld = m->d;
+    go.epi.n_valid = m->d;
+    HIP_TRY(launch_gemm(m->wtype, mt, go, s));
+
+    HIP_TRY(launch_rmsnorm_pack(m->x, M, m->d, lw.ffn_norm, m->cfg.rms_eps, m->wtype, m->pk_d,
+                                nullptr, s));
+    // gate/up + SwiGLU into the down-projection pack
+    GemmArgs gu{};
+    gu.M = M;
+    gu.W = lw.wgu;
+    gu.Xhi = m->pk_d.hi;
+    gu.Xlo = m->pk_d.lo;
+    gu.Nb = m->Nb_gu;
+    gu.Kb = m->Kb_d;
+    gu.epi.kind = EPI_SILU;
+    gu.epi.pack = m->pk_ff;
+    gu.epi.ff = m->ff;
+    HIP_TRY(launch_gemm(m->wtype, mt, gu, s));
+    // down + residual
+    GemmArgs gd{};
+    gd.M = M;
+    gd.W = lw.wdown;
+    gd.Xhi = m->pk_ff.hi;
+    gd.Xlo = m->pk_ff.lo;
+    gd.Nb = m->Nb_down;
+    gd.Kb = m->Kb_ff;
+    gd.epi.kind = EPI_RESID;
+    gd.epi.out = m->x;
+    gd.epi.ld = m->d;
+    gd.epi.n_valid = m->d;
+    HIP_TRY(launch_gemm(m->wtype, mt, gd, s));
+
+    if (l + 1 < m->L) {
+      HIP_TRY(launch_rmsnorm_pack(m->x, M, m->d, m->layers[l + 1].attn_norm, m->cfg.rms_eps,
+                                  m->wtype, m->pk_d, hidden ? hidden + (size_t)(l + 1) * Md : nullptr,
+                                  s));
+    }
+  }
+  if (hidden && !logits)
+    HIP_TRY(launch_copy_rows(m->x, hidden + (size_t)m->L * Md, Md, s));
+  if (!logits) return DSI_OK;
+
+  GemmArgs gh{};
+  gh.W = m->lm_head;
+  gh.Xhi = m->pk_d.hi;
+  gh.Xlo = m->pk_d.lo;
+  gh.Nb = m->Nb_head;
+  gh.Kb = m->Kb_d;
+  gh.epi.kind = EPI_STORE;
+  gh.epi.out = logits;
+  gh.epi.ld = m->V;
+  gh.epi.n_valid = m->V;
+  if (head_last_only) {
+    HIP_TRY(launch_rmsnorm_pack(m->x + (size_t)(M - 1) * m->d, 1, m->d, m->final_norm,
+                                m->cfg.rms_eps, m->wtype, m->pk_d, nullptr, s));
+    gh.M = 1;
+    HIP_TRY(launch_gemm(m->wtype, 1, gh, s));
+  } else {
+    HIP_TRY(launch_rmsnorm_pack(m->x, M, m->d, m->final_norm, m->cfg.rms_eps, m->wtype, m->pk_d,
+                                hidden ? hidden + (size_t)m->L * Md : nullptr, s));
+    gh.M = M;
+    HIP_TRY(launch_gemm(m->wtype, mt, gh, s));
+  }
+  return DSI_OK;
+}
+
+// library workspace for dsi_accept, one per device
+struct AcceptWs {
+  DevBuf ws;
+  int* err = nullptr;
+};
+std::mutex g_accept_mu;
+std::map<int, AcceptWs> g_accept;
+
+dsi_status check_err_word(int* err, hipStream_t s) {
+  HIP_TRY(hipStreamSynchronize(s));
+  int h = 0;
+  HIP_TRY(hipMemcpy(&h, err, sizeof(int), hipMemcpyDeviceToHost));
+  if (h) {
+    HIP_TRY(hipMemset(err, 0, sizeof(int)));
+    std::string what;
+    if (h & 1) what += " token id outside [0, vocab);";
+    if (h & 2) what += " verification input invalid (token id or q(d) <= 0);";
+    if (h & 4) what += " rollback above the current length;";
+    return fail(DSI_EINVAL, "device-detected input error:%s", what.c_str());
+  }
+  return DSI_OK;
+}
+
+dsi_status verify_args_ok(int B, int k, int V, const int* tokens, const float* q, const float* u,
+                          float T, int mode, const int* n_out, const int* tok_out) {
+  if (B < 1) return fail(DSI_EINVAL, "n_windows must be >= 1");
+  if (k < 0) return fail(DSI_EINVAL, "k must be >= 0");
+  if ((long long)B * (k + 1) > DSI_MAX_ROWS)
+    return fail(DSI_EINVAL, "n_windows*(k+1) = %lld exceeds %d", (long long)B * (k + 1), DSI_MAX_ROWS);
+  if (!tokens || !n_out || !tok_out) return fail(DSI_EINVAL, "null tokens or output pointer");
+  if (mode != DSI_SAMPLE && mode != DSI_GREEDY) return fail(DSI_EINVAL, "bad mode %d", mode);
+  if (mode == DSI_SAMPLE) {
+    if (!u) return fail(DSI_EINVAL, "sample mode needs d_u");
+    if (k > 0 && !q) return fail(DSI_EINVAL, "sample mode needs d_q");
+    if (!(T > 0.f) || !isfinite(T)) return fail(DSI_EINVAL, "temperature must be positive");
+  }
+  if (V < 1) return fail(DSI_EINVAL, "vocab must be >= 1");
+  return DSI_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* dsi_last_error(void) { return g_err.c_str(); }
+
+dsi_status dsi_model_create(const dsi_config* cfg, void* stream, dsi_model** out) {
+  if (!cfg || !out) return fail(DSI_EINVAL, "null argument");
+  const dsi_config c = *cfg;
+  if (c.n_layers < 1 || c.d_model < 32 || c.d_model % 32 || c.n_heads < 1 || c.n_kv_heads < 1 ||
+      c.n_heads % c.n_kv_heads || c.d_ff < 1 || c.vocab < 1)
+    return fail(DSI_EINVAL, "invalid shape (d_model must be a multiple of 32)");
+  if (c.head_dim != 32 && c.head_dim != 64 && c.head_dim != 96 && c.head_dim != 128)
+    return fail(DSI_EINVAL, "head_dim must be 32, 64, 96 or 128");
+  if ((c.wdtype != DSI_F32 && c.wdtype != DSI_BF16) || (c.kvdtype != DSI_F32 && c.kvdtype != DSI_BF16))
+    return fail(DSI_EINVAL, "bad dtype");
+  if (!(c.rms_eps >= 0.f) || !(c.rope_base > 0.f)) return fail(DSI_EINVAL, "bad eps / rope_base");
+  dsi_model* m = new (std::nothrow) dsi_model();
+  if (!m) return fail(DSI_ENOMEM, "host allocation failed");
+  m->cfg = c;
+  m->stream = (hipStream_t)stream;
+  m->wtype = c.wdtype == DSI_BF16 ? W_BF16 : W_F32;
+  m->kvb = c.kvdtype == DSI_BF16 ? 1 : 0;
+  m->esz = m->wtype == W_BF16 ? 2 : 4;
+  m->kvesz = m->kvb ? 2 : 4;
+  m->d = c.d_model;
+  m->hq = c.n_heads;
+  m->hkv = c.n_kv_heads;
+  m->hd = c.head_dim;
+  m->qdim = c.n_heads * c.head_dim;
+  m->kvdim = c.n_kv_heads * c.head_dim;
+  m->ff = c.d_ff;
+  m->V = c.vocab;
+  m->L = c.n_layers;
+  m->Kb_d = m->d / 32;
+  m->Kb_q = m->qdim / 32;
+  m->Kb_ff = cdiv(m->ff, 32);
+  m->Nb_qkv = (m->qdim + 2 * m->kvdim) / 16;
+  m->Nb_o = m->d / 16;
+  m->Nb_gu = cdiv(m->ff, 8);
+  m->Nb_down = m->d / 16;
+  m->Nb_head = cdiv(m->V, 16);
+  m->layers.resize(m->L);
+  m->set_mask.assign(m->L + 1, 0u);
+
+  dsi_status st = DSI_OK;
+  auto A = [&](void** p, size_t bytes) {
+    if (st == DSI_OK) st = dev_alloc(m->allocs, p, bytes);
+  };
+  const size_t tile = 512;
+  A(&m->embed, (size_t)m->V * m->d * m->esz);
+  A((void**)&m->final_norm, (size_t)m->d * 4);
+  A(&m->lm_head, (size_t)m->Nb_head * m->Kb_d * tile * m->esz);
+  for (int l = 0; l < m->L && st == DSI_OK; ++l) {
+    LayerW& w = m->layers[l];
+    A((void**)&w.attn_norm, (size_t)m->d * 4);
+    A((void**)&w.ffn_norm, (size_t)m->d * 4);
+    A(&w.wqkv, (size_t)m->Nb_qkv * m->Kb_d * tile * m->esz);
+    A(&w.wo, (size_t)m->Nb_o * m->Kb_q * tile * m->esz);
+    A(&w.wgu, (size_t)m->Nb_gu * m->Kb_d * tile * m->esz);
+    A(&w.wdown, (size_t)m->Nb_down * m->Kb_ff * tile * m->esz);
+  }
+  A((void**)&m->x, (size_t)kMaxRows * m->d * 4);
+  if (st == DSI_OK) m->pk_d = make_pack(m, m->Kb_d, &st);
+  if (st == DSI_OK) m->pk_q = make_pack(m, m->Kb_q, &st);
+  if (st == DSI_OK) m->pk_ff = make_pack(m, m->Kb_ff, &st);
+  A((void**)&m->qbuf, (size_t)kMaxRows * m->qdim * 4);
+  A((void**)&m->rope, (size_t)kMaxRows * (m->hd / 2) * sizeof(float2));
+  A((void**)&m->logits, (size_t)kMaxRows * m->V * 4);
+  A(&m->vws, verify_workspace_bytes(kMaxRows, kMaxRows, m->V));
+  A((void**)&m->err, 64);
+  if (st != DSI_OK) {
+    free_list(m->allocs);
+    delete m;
+    return st;
+  }
+  *out = m;
+  return DSI_OK;
+}
+
+dsi_status dsi_model_destroy(dsi_model* m) {
+  if (!m) return DSI_OK;
+  if (m->live_kv) return fail(DSI_ESTATE, "destroy the model's KV caches first");
+  hipStreamSynchronize(m->stream);
+  free_list(m->allocs);
+  if (m->attn_o.p) hipFree(m->attn_o.p);
+  if (m->attn_ml.p) hipFree(m->attn_ml.p);
+  delete m;
+  return DSI_OK;
+}
+
+dsi_status dsi_model_set_tensor(dsi_model* m, int32_t layer, int32_t id, const void* src, size_t nbytes,
+                                int32_t src_on_device) {
+  if (!m || !src) return fail(DSI_EINVAL, "null argument");
+  const bool global = id == DSI_T_EMBED || id == DSI_T_FINAL_NORM || id == DSI_T_LM_HEAD;
+  if (id < 0 || id > DSI_T_W_DOWN) return fail(DSI_EINVAL, "bad tensor id %d", id);
+  if (global ? layer != -1 : (layer < 0 || layer >= m->L))
+    return fail(DSI_EINVAL, "bad layer %d for tensor %d", layer, id);
+  size_t rows = 1, cols = 1;
+  switch (id) {
+    case DSI_T_EMBED: case DSI_T_LM_HEAD: rows = m->V; cols = m->d; break;
+    case DSI_T_FINAL_NORM: case DSI_T_ATTN_NORM: case DSI_T_FFN_NORM: rows = 1; cols = m->d; break;
+    case DSI_T_WQ: rows = m->qdim; cols = m->d; break;
+    case DSI_T_WK: case DSI_T_WV: rows = m->kvdim; cols = m->d; break;
+    case DSI_T_WO: rows = m->d; cols = m->qdim; break;
+    case DSI_T_W_GATE: case DSI_T_W_UP: rows = m->ff; cols = m->d; break;
+    case DSI_T_W_DOWN: rows = m->d; cols = m->ff; break;
+  }
+  if (nbytes != rows * cols * m->esz)
+    return fail(DSI_EINVAL, "tensor %d: expected %zu bytes, got %zu", id, rows * cols * m->esz, nbytes);
+  const hipMemcpyKind kind = src_on_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice;
+
+  if (id == DSI_T_FINAL_NORM || id == DSI_T_ATTN_NORM || id == DSI_T_FFN_NORM) {
+    std::vector<unsigned char> hbuf(nbytes);
+    if (src_on_device) HIP_TRY(hipMemcpy(hbuf.data(), src, nbytes, hipMemcpyDeviceToHost));
+    else memcpy(hbuf.data(), src, nbytes);
+    std::vector<float> g(m->d);
+    for (int i = 0; i < m->d; ++i) {
+      if (m->wtype == W_BF16) {
+        uint16_t b;
+        memcpy(&b, hbuf.data() + 2 * i, 2);
+        uint32_t u = (uint32_t)b << 16;
+        memcpy(&g[i], &u, 4);
+      } else {
+        memcpy(&g[i], hbuf.data() + 4 * i, 4);
+      }
+    }
+    float* dst = id == DSI_T_FINAL_NORM ? m->final_norm
+                 : id == DSI_T_ATTN_NORM ? m->layers[layer].attn_norm : m->layers[layer].ffn_norm;
+    HIP_TRY(hipMemcpy(dst, g.data(), (size_t)m->d * 4, hipMemcpyHostToDevice));
+  } else if (id == DSI_T_EMBED) {
+    HIP_TRY(hipMemcpy(m->embed, src, nbytes, kind));
+  } else {
+    const void* dsrc = src;
+    void* staging = nullptr;
+    if (!src_on_device) {
+      hipError_t e = hipMalloc(&staging, nbytes);
+      if (e != hipSuccess) {
+        hipGetLastError();
+        return fail(DSI_ENOMEM, "staging hipMalloc(%zu) failed", nbytes);
+      }
+      e = hipMemcpy(staging, src, nbytes, hipMemcpyHostToDevice);
+      if (e != hipSuccess) {
+        hipFree(staging);
+        return fail(DSI_EHIP, "hipMemcpy: %s", hipGetErrorString(e));
+      }
+      dsrc = staging;
+    }
+    hipError_t e = hipSuccess;
+    LayerW* lw = global ? nullptr : &m->layers[layer];
+    const int nq = m->qdim / 16, nk = m->kvdim / 16;
+    switch (id) {
+      case DSI_T_LM_HEAD: e = launch_prepack(m->wtype, dsrc, m->V, m->d, m->lm_head, m->Kb_d, 0, 0, m->hd, 0, nullptr); break;
+      case DSI_T_WQ: e = launch_prepack(m->wtype, dsrc, m->qdim, m->d, lw->wqkv, m->Kb_d, 0, 1, m->hd, 0, nullptr); break;
+      case DSI_T_WK: e = launch_prepack(m->wtype, dsrc, m->kvdim, m->d, lw->wqkv, m->Kb_d, nq, 1, m->hd, 0, nullptr); break;
+      case DSI_T_WV: e = launch_prepack(m->wtype, dsrc, m->kvdim, m->d, lw->wqkv, m->Kb_d, nq + nk, 0, m->hd, 0, nullptr); break;
+      case DSI_T_WO: e = launch_prepack(m->wtype, dsrc, m->d, m->qdim, lw->wo, m->Kb_q, 0, 0, m->hd, 0, nullptr); break;
+      case DSI_T_W_GATE: e = launch_prepack(m->wtype, dsrc, m->ff, m->d, lw->wgu, m->Kb_d, 0, 2, m->hd, 0, nullptr); break;
+      case DSI_T_W_UP: e = launch_prepack(m->wtype, dsrc, m->ff, m->d, lw->wgu, m->Kb_d, 0, 2, m->hd, 1, nullptr); break;
+      case DSI_T_W_DOWN: e = launch_prepack(m->wtype, dsrc, m->d, m->ff, lw->wdown, m->Kb_ff, 0, 0, m->hd, 0, nullptr); break;
+    }
+    if (e == hipSuccess) e = hipDeviceSynchronize();
+    if (staging) hipFree(staging);
+    if (e != hipSuccess) return fail(DSI_EHIP, "prepack: %s", hipGetErrorString(e));
+  }
+  m->set_mask[global ? 0 : layer + 1] |= 1u << id;
+  return DSI_OK;
+}
+
+dsi_status dsi_kv_create(dsi_model* m, int32_t n_windows, int32_t max_len, dsi_kv** out) {
+  if (!m || !out) return fail(DSI_EINVAL, "null argument");
+  if (n_windows < 1 || max_len < 1) return fail(DSI_EINVAL, "n_windows and max_len must be >= 1");
+  dsi_kv* kv = new (std::nothrow) dsi_kv();
+  if (!kv) return fail(DSI_ENOMEM, "host allocation failed");
+  kv->m = m;
+  kv->n_windows = n_windows;
+  kv->max_len = max_len;
+  kv->maxlen_pad = (int)round_up((size_t)max_len, 64);
+  kv->win_elems = (size_t)m->hkv * kv->maxlen_pad * m->hd;
+  kv->hi.assign(n_windows, 0);
+  kv->lo.assign(n_windows, 0);
+  const size_t bytes = (size_t)m->L * n_windows * kv->win_elems * m->kvesz;
+  std::vector<void*> list;
+  dsi_status st = dev_alloc(list, &kv->k, bytes);
+  if (st == DSI_OK) st = dev_alloc(list, &kv->v, bytes);
+  if (st == DSI_OK) st = dev_alloc(list, (void**)&kv->lens, (size_t)n_windows * sizeof(int));
+  if (st != DSI_OK) {
+    free_list(list);
+    delete kv;
+    return st;
+  }
+  m->live_kv++;
+  *out = kv;
+  return DSI_OK;
+}
+
+dsi_status dsi_kv_destroy(dsi_kv* kv) {
+  if (!kv) return DSI_OK;
+  hipStreamSynchronize(kv->m->stream);
+  hipFree(kv->k);
+  hipFree(kv->v);
+  hipFree(kv->lens);
+  kv->m->live_kv--;
+  delete kv;
+  return DSI_OK;
+}
+
+dsi_status dsi_prefill(dsi_model* m, dsi_kv* kv, int32_t window, const int32_t* d_tokens, int32_t n,
+                       float* d_last_logits) {
+  if (!m || !kv || kv->m != m) return fail(DSI_EINVAL, "model / kv mismatch");
+  if (window < 0 || window >= kv->n_windows) return fail(DSI_EINVAL, "bad window %d", window);
+  if (n < 0 || (n > 0 && !d_tokens)) return fail(DSI_EINVAL, "bad token count / pointer");
+  if (!all_set(m)) return fail(DSI_ESTATE, "not every model tensor has been set");
+  if (kv->hi[window] + n > kv->max_len)
+    return fail(DSI_ECAPACITY, "window %d: length (<= %lld) + %d exceeds max_len %d", window,
+                kv->hi[window], n, kv->max_len);
+  for (int off = 0; off < n; off += kMaxRows) {
+    const int rows = std::min(kMaxRows, n - off);
+    const bool last = off + rows == n;
+    DSI_TRY(run_forward(m, kv, window, 1, rows, d_tokens + off, last ? d_last_logits : nullptr, 1,
+                        nullptr));
+    HIP_TRY(launch_kv_add_checked(kv->lens, window, d_tokens + off, rows, m->V, m->err, m->stream));
+    kv->hi[window] += rows;
+  }
+  return DSI_OK;
+}
+
+dsi_status dsi_verify(dsi_model* m, dsi_kv* kv, const dsi_verify_args* a, int32_t* d_n_accepted,
+                      int32_t* d_next_token) {
+  if (!m || !kv || !a || kv->m != m) return fail(DSI_EINVAL, "null argument or model / kv mismatch");
+  const int B = a->n_windows, k = a->k;
+  DSI_TRY(verify_args_ok(B, k, m->V, a->d_tokens, a->d_q, a->d_u, a->temperature, a->mode,
+                         d_n_accepted, d_next_token));
+  if (a->window0 < 0 || a->window0 + B > kv->n_windows)
+    return fail(DSI_EINVAL, "windows [%d, %d) outside the cache's %d", a->window0, a->window0 + B,
+                kv->n_windows);
+  if (!all_set(m)) return fail(DSI_ESTATE, "not every model tensor has been set");
+  for (int b = 0; b < B; ++b)
+    if (kv->hi[a->window0 + b] + k + 1 > kv->max_len)
+      return fail(DSI_ECAPACITY, "window %d: length (<= %lld) + %d exceeds max_len %d", a->window0 + b,
+                  kv->hi[a->window0 + b], k + 1, kv->max_len);
+  float* logits = a->d_logits_out ? a->d_logits_out : m->logits;
+  DSI_TRY(run_forward(m, kv, a->window0, B, k + 1, a->d_tokens, logits, 0, a->d_hidden_out));
+  VerifyArgs va{};
+  va.B = B;
+  va.k = k;
+  va.V = m->V;
+  va.logits = logits;
+  va.tokens = a->d_tokens;
+  va.q = a->d_q;
+  va.u = a->d_u;
+  va.temperature = (double)a->temperature;
+  va.greedy = a->mode == DSI_GREEDY;
+  va.commit = a->commit;
+  va.lens = kv->lens;
+  va.window0 = a->window0;
+  va.n_out = d_n_accepted;
+  va.tok_out = d_next_token;
+  va.err = m->err;
+  verify_bind_workspace(va, m->vws, B * (k + 1), B, m->V);
+  HIP_TRY(launch_verify(va, m->stream));
+  if (a->commit)
+    for (int b = 0; b < B; ++b) kv->hi[a->window0 + b] += k + 1;
+  return DSI_OK;
+}
+
+dsi_status dsi_accept(void* stream, int32_t B, int32_t k, int32_t V, const float* d_logits,
+                      const int32_t* d_tokens, const float* d_q, const float* d_u, float temperature,
+                      int32_t mode, int32_t* d_n_accepted, int32_t* d_next_token) {
+  DSI_TRY(verify_args_ok(B, k, V, d_tokens, d_q, d_u, temperature, mode, d_n_accepted, d_next_token));
+  if (!d_logits) return fail(DSI_EINVAL, "null logits");
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  std::lock_guard<std::mutex> lk(g_accept_mu);
+  AcceptWs& w = g_accept[dev];
+  if (!w.err) {
+    hipError_t e = hipMalloc((void**)&w.err, 64);
+    if (e != hipSuccess) {
+      hipGetLastError();
+      w.err = nullptr;
+      return fail(DSI_ENOMEM, "hipMalloc failed");
+    }
+    HIP_TRY(hipMemset(w.err, 0, 64));
+  }
+  DSI_TRY(ensure(w.ws, verify_workspace_bytes(B * (k + 1), B, V)));
+  VerifyArgs va{};
+  va.B = B;
+  va.k = k;
+  va.V = V;
+  va.logits = d_logits;
+  va.tokens = d_tokens;
+  va.q = d_q;
+  va.u = d_u;
+  va.temperature = (double)temperature;
+  va.greedy = mode == DSI_GREEDY;
+  va.commit = 0;
+  va.lens = nullptr;
+  va.window0 = 0;
+  va.n_out = d_n_accepted;
+  va.tok_out = d_next_token;
+  va.err = w.err;
+  verify_bind_workspace(va, w.ws.p, B * (k + 1), B, V);
+  HIP_TRY(launch_verify(va, (hipStream_t)stream));
+  return DSI_OK;
+}
+
+dsi_status dsi_kv_rollback(dsi_kv* kv, int32_t window, int32_t new_len) {
+  if (!kv) return fail(DSI_EINVAL, "null kv");
+  if (window < 0 || window >= kv->n_windows) return fail(DSI_EINVAL, "bad window %d", window);
+  if (new_len < 0 || new_len > kv->hi[window])
+    return fail(DSI_EINVAL, "rollback to %d above the window's length (<= %lld)", new_len, kv->hi[window]);
+  HIP_TRY(launch_kv_rollback(kv->lens, window, new_len, kv->m->err, kv->m->stream));
+  kv->hi[window] = new_len;
+  kv->lo[window] = std::min(kv->lo[window], (long long)new_len);
+  return DSI_OK;
+}
+
+dsi_status dsi_kv_length(dsi_kv* kv, int32_t window, int32_t* len) {
+  if (!kv || !len) return fail(DSI_EINVAL, "null argument");
+  if (window < 0 || window >= kv->n_windows) return fail(DSI_EINVAL, "bad window %d", window);
+  HIP_TRY(hipStreamSynchronize(kv->m->stream));
+  int h = 0;
+  HIP_TRY(hipMemcpy(&h, kv->lens + window, sizeof(int), hipMemcpyDeviceToHost));
+  *len = h;
+  kv->hi[window] = kv->lo[window] = h;
+  return check_err_word(kv->m->err, kv->m->stream);
+}
+
+dsi_status dsi_sync(dsi_model* m) {
+  if (!m) return fail(DSI_EINVAL, "null model");
+  return check_err_word(m->err, m->stream);
+}
+
+static dsi_status kv_copy(dsi_kv* kv, int32_t window, int32_t layer, int32_t len, void* dk, void* dv,
+                          int to_cache) {
+  if (!kv || !dk || !dv) return fail(DSI_EINVAL, "null argument");
+  dsi_model* m = kv->m;
+  if (window < 0 || window >= kv->n_windows || layer < 0 || layer >= m->L || len < 0 || len > kv->max_len)
+    return fail(DSI_EINVAL, "bad window / layer / len");
+  HIP_TRY(launch_kv_copy(to_cache, m->kvb, kv_ptr(kv, kv->k, layer, window), kv_ptr(kv, kv->v, layer, window),
+                         m->hkv, m->hd, kv->maxlen_pad, len, dk, dv, m->stream));
+  return DSI_OK;
+}
+
+dsi_status dsi_kv_export(dsi_kv* kv, int32_t window, int32_t layer, int32_t len, void* d_k, void* d_v) {
+  return kv_copy(kv, window, layer, len, d_k, d_v, 0);
+}
+
+dsi_status dsi_kv_import(dsi_kv* kv, int32_t window, int32_t layer, int32_t len, const void* d_k,
+                         const void* d_v) {
+  return kv_copy(kv, window, layer, len, (void*)d_k, (void*)d_v, 1);
+}
+
+dsi_status dsi_kv_set_length(dsi_kv* kv, int32_t window, int32_t len) {
+  if (!kv) return fail(DSI_EINVAL, "null kv");
+  if (window < 0 || window >= kv->n_windows || len < 0 || len > kv->max_len)
+    return fail(DSI_EINVAL, "bad window / len");
+  HIP_TRY(launch_kv_set(kv->lens, window, len, kv->m->stream));
+  kv->hi[window] = kv->lo[window] = len;
+  return DSI_OK;
+}
+
+}  // extern "C"

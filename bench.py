@@ -1,0 +1,316 @@
+"""Benchmark of one DSI verification step on one MI355X.
+
+A step is one dsi_verify (target forward over the k+1 window rows of every
+window against its cached prefix, accept/reject, KV commit) followed by the
+dsi_kv_rollback that restores the prefix length, on synthetic random-init
+weights and inputs (dsi_synth).  Prints ONE JSON line.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+Default workload: the Llama-style 8B shape (32 layers, d 4096, 32/8 heads,
+head_dim 128, SwiGLU 14336, vocab 128256) in bf16, prefix 2048, k = 10, one
+window, sampling mode at temperature 1.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import threading
+import time
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import dsi_synth as S  # noqa: E402
+
+METRIC = "verify-step latency (ms) + verified draft tokens/s, 8B-shape k=10; % HBM peak"
+HBM_PEAK_GBS = 8000.0
+SEED = 0
+
+
+def log(msg: str):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+# ------------------------------------------------------------ byte accounting
+def step_bytes(shape, prefix_lens, k) -> dict:
+    """Algorithmic HBM bytes of one verification step: every linear and
+    LM-head weight once, norm gains, embedding rows, KV reads of each
+    window's keys [0, L_b + k], KV writes of the window rows, the logits
+    written and read, and q (k scalars + V entries of one residual row)."""
+    s = shape
+    B = len(prefix_lens)
+    M = B * (k + 1)
+    esz = 2 if s.wdtype == "bf16" else 4
+    kvsz = 2 if s.kvdtype == "bf16" else 4
+    lin = s.d_model * (s.q_dim + 2 * s.kv_dim) + s.q_dim * s.d_model + 3 * s.d_model * s.d_ff
+    weights = (s.n_layers * lin + s.vocab * s.d_model) * esz
+    gains = (2 * s.n_layers + 1) * s.d_model * 4
+    embed = M * s.d_model * esz
+    kv_read = sum(L + k + 1 for L in prefix_lens) * 2 * s.kv_dim * kvsz * s.n_layers
+    kv_write = M * 2 * s.kv_dim * kvsz * s.n_layers
+    logits = 2 * M * s.vocab * 4
+    q = B * (k + s.vocab) * 4
+    total = weights + gains + embed + kv_read + kv_write + logits + q
+    return {"total": total, "weights": weights, "kv_read": kv_read}
+
+
+def gateup_bytes(shape, M) -> int:
+    """Algorithmic bytes of one gate/up launch: both weight matrices, the
+    normalised input rows (fp32-equivalent) and the SwiGLU output rows."""
+    esz = 2 if shape.wdtype == "bf16" else 4
+    return 2 * shape.d_ff * shape.d_model * esz + M * shape.d_model * 4 + M * shape.d_ff * 4
+
+
+# ------------------------------------------------------------------ GPU part
+def build_model(dsi, loader, shape, stream, n_windows, max_len):
+    model = dsi.dsi_model_create(loader.config_for(shape), stream)
+    names = [(-1, n) for n in S.GLOBAL_TENSORS] + [(l, n) for l in range(shape.n_layers)
+                                                    for n in S.LAYER_TENSORS]
+
+    def make(item):
+        l, n = item
+        w = S.weight(shape, SEED, l, n)
+        return S.f32_to_bf16_bits(w) if shape.wdtype == "bf16" else w
+
+    t0 = time.time()
+    # generate the next tensor on a helper thread while the current uploads
+    with ThreadPoolExecutor(2) as ex:
+        fut = ex.submit(make, names[0])
+        for i, (l, n) in enumerate(names):
+            a = np.ascontiguousarray(fut.result())
+            if i + 1 < len(names):
+                fut = ex.submit(make, names[i + 1])
+            dsi.dsi_model_set_tensor(model, l, dsi.TENSOR_IDS[n], a.ctypes.data, a.nbytes, False)
+            if l >= 0 and n == "w_down" and (l + 1) % 8 == 0:
+                log(f"uploaded layer {l + 1}/{shape.n_layers} ({time.time() - t0:.1f}s)")
+    kv = dsi.dsi_kv_create(model, n_windows, max_len)
+    return model, kv
+
+
+def run_gpu(args, wl):
+    import torch
+    from paper_2405_14105_amd import dsi, loader
+
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a GPU (cuda:0)")
+    dsi.load()
+    dev = torch.device("cuda:0")
+    shape, k, lens = wl.shape, wl.k, list(wl.prefix_lens)
+    B = len(lens)
+    stream = torch.cuda.current_stream().cuda_stream
+    if args.copy_calibration:
+        a = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+        b = torch.empty_like(a)
+        a.fill_(1)
+        torch.cuda.synchronize()
+        b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+        log("copy calibration: 512 MiB device-to-device copy done")
+    t0 = time.time()
+    model, kv = build_model(dsi, loader, shape, stream, B, max(lens) + k + 1)
+    log(f"model ready in {time.time() - t0:.1f}s")
+    t1 = time.time()
+    for b, L in enumerate(lens):
+        pt = torch.from_numpy(S.prefix_tokens(shape, SEED, b, L)).to(dev)
+        dsi.dsi_prefill(model, kv, b, pt, L, None)
+    torch.cuda.synchronize()
+    log(f"prefill of {sum(lens)} tokens in {time.time() - t1:.1f}s")
+    wi = S.window_inputs(shape, SEED, B, k)
+    tok = torch.from_numpy(wi["tokens"]).to(dev)
+    q = torch.from_numpy(wi["q"]).to(dev)
+    u = torch.from_numpy(wi["u"]).to(dev)
+    n_out = torch.empty(B, dtype=torch.int32, device=dev)
+    t_out = torch.empty(B, dtype=torch.int32, device=dev)
+    mode = dsi.DSI_GREEDY if args.mode == "greedy" else dsi.DSI_SAMPLE
+
+    def step():
+        dsi.dsi_verify(model, kv, 0, B, k, tok, q, u, n_out, t_out, wl.temperature, mode, True)
+        for b, L in enumerate(lens):
+            dsi.dsi_kv_rollback(kv, b, L)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    dsi.dsi_sync(model)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    torch.cuda.synchronize()
+    wall0 = time.time()
+    for i in range(args.steps):
+        evs[i].record()
+        step()
+    evs[-1].record()
+    torch.cuda.synchronize()
+    wall = time.time() - wall0
+    per = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)])
+    total_ms = evs[0].elapsed_time(evs[-1])
+    ms = total_ms / args.steps
+    n_acc = n_out.cpu().numpy()
+    log(f"timed {args.steps} steps: {ms:.4f} ms/step (p50 {np.median(per):.4f}), wall {wall:.2f}s, "
+        f"n = {n_acc.tolist()}")
+
+    if args.no_kernel_pass:
+        dsi.dsi_kv_destroy(kv)
+        dsi.dsi_model_destroy(model)
+        return {"ms": ms, "per_step": per, "kernels": None, "n_accepted": n_acc.tolist()}
+    # kernel-class timing pass: event pairs around every launch of each class
+    classes = {"qkv": dsi.DSI_K_QKV, "attention": dsi.DSI_K_ATTN, "o_proj": dsi.DSI_K_OPROJ,
+               "gate_up": dsi.DSI_K_GATEUP, "down": dsi.DSI_K_DOWN, "head": dsi.DSI_K_HEAD,
+               "verify": dsi.DSI_K_VERIFY}
+    kt = {}
+    for name, cls in classes.items():
+        dsi.dsi_profile_begin(model, cls)
+        for _ in range(args.steps):
+            step()
+        nl, tot = dsi.dsi_profile_end(model)
+        kt[name] = {"launches_per_step": nl / args.steps, "avg_ms": tot / max(nl, 1),
+                    "ms_per_step": tot / args.steps}
+    log("per-class ms/step: " + ", ".join(f"{n} {v['ms_per_step']:.3f}" for n, v in kt.items()))
+    dsi.dsi_kv_destroy(kv)
+    dsi.dsi_model_destroy(model)
+    return {"ms": ms, "per_step": per, "kernels": kt, "n_accepted": n_acc.tolist()}
+
+
+# ------------------------------------------------------------ CPU baseline
+def cpu_baseline(wl, sample_layers: int):
+    """The fp64 oracle on the host: `sample_layers` decoder layers over the
+    window rows against an fp64 prefix cache of the full length, the final
+    norm + LM head, and verify64 for every window; the per-layer time is
+    scaled to the full depth."""
+    from oracle import layer64, head64, verify64
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        cores = os.cpu_count() or 1
+    s, k, lens = wl.shape, wl.k, list(wl.prefix_lens)
+    B = len(lens)
+    rng = np.random.default_rng(1)
+    wi = S.window_inputs(s, SEED, B, k)
+    layers = list(range(sample_layers))
+    cache = {}
+
+    def get(layer, name):
+        if (layer, name) not in cache:
+            cache[(layer, name)] = S.weight(s, SEED, layer, name).astype(np.float64)
+        return cache[(layer, name)]
+
+    for l in layers:
+        for n in S.LAYER_TENSORS:
+            get(l, n)
+    for n in S.GLOBAL_TENSORS:
+        get(-1, n)
+    kvs = [(rng.standard_normal((L, s.n_kv_heads, s.head_dim)) * 0.5,
+            rng.standard_normal((L, s.n_kv_heads, s.head_dim)) * 0.5) for L in lens]
+    x0 = [get(-1, "embed")[wi["tokens"][b]] for b in range(B)]
+
+    def one():
+        t_layers = 0.0
+        t_rest = 0.0
+        for b, L in enumerate(lens):
+            pos = np.arange(L, L + k + 1)
+            x = x0[b]
+            ta = time.perf_counter()
+            for l in layers:
+                x, _, _ = layer64(s, get, l, x, pos, kvs[b][0], kvs[b][1])
+            tb = time.perf_counter()
+            z = head64(s, get, x)
+            verify64(z, wi["tokens"][b, 1:], wi["q"][b], wi["u"][b], wl.temperature)
+            tc = time.perf_counter()
+            t_layers += tb - ta
+            t_rest += tc - tb
+        return t_layers / len(layers) * s.n_layers + t_rest
+
+    times = [one() for _ in range(3)]
+    t = float(np.median(times))
+    return {
+        "value": B * k / t,
+        "unit": "verified draft tokens/s",
+        "cores": int(cores),
+        "kind": "oracle",
+        "sample": (f"fp64 oracle: {sample_layers} of {s.n_layers} decoder layers over the {k + 1} "
+                   f"window rows of each of {B} window(s) against a random fp64 prefix cache of the "
+                   f"full length, plus final norm + LM head + verify64; per-layer time scaled to "
+                   f"{s.n_layers} layers; median of 3 ({t * 1e3:.1f} ms per step estimated)"),
+        "step_ms_estimated": t * 1e3,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llama8b_L2048_k10", choices=sorted(S.WORKLOADS))
+    ap.add_argument("--mode", default="sample", choices=["sample", "greedy"])
+    ap.add_argument("--cpu-sample-layers", type=int, default=2)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-kernel-pass", action="store_true",
+                    help="skip the per-class event timing pass (for counter runs)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run one 512 MiB device copy first (counter scale reference)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: this verification step is a single-GPU kernel path "
+              f"(--gpus {args.gpus} requested); concurrent verification tasks are batched "
+              f"windows on one GPU (workload llama8b_x7_L1024_k5).", file=sys.stderr)
+        sys.exit(2)
+    wl = S.WORKLOADS[args.workload]
+    g = run_gpu(args, wl)
+    sb = step_bytes(wl.shape, wl.prefix_lens, wl.k)
+    ms = g["ms"]
+    B, k = wl.n_windows, wl.k
+    M = B * (k + 1)
+    if g["kernels"] is None:
+        print(json.dumps({"metric": METRIC, "ms_per_step": round(ms, 4), "note": "counter run"}))
+        return
+    gu = g["kernels"]["gate_up"]
+    gu_bytes = gateup_bytes(wl.shape, M)
+    achieved = gu_bytes / (gu["avg_ms"] * 1e-3) / 1e9
+    roof = {"bound": "hbm", "kernel": "gate/up projection + SwiGLU (k_gemm_bf16 EPI_SILU)",
+            "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+            "bytes_per_launch": gu_bytes, "avg_launch_ms": round(gu["avg_ms"], 5)}
+    out = {
+        "metric": METRIC,
+        "value": round(B * k / (ms * 1e-3), 1),
+        "unit": "verified draft tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.shape.wdtype,
+        "data": "synthetic",
+        "config": {"workload": wl.name, "layers": wl.shape.n_layers, "d_model": wl.shape.d_model,
+                   "heads": wl.shape.n_heads, "kv_heads": wl.shape.n_kv_heads,
+                   "head_dim": wl.shape.head_dim, "d_ff": wl.shape.d_ff, "vocab": wl.shape.vocab,
+                   "prefix": list(wl.prefix_lens), "k": k, "windows": B, "mode": args.mode,
+                   "temperature": wl.temperature},
+        "latency_ms": {"p10": round(float(np.percentile(g["per_step"], 10)), 4),
+                       "p50": round(float(np.percentile(g["per_step"], 50)), 4),
+                       "p90": round(float(np.percentile(g["per_step"], 90)), 4)},
+        "step_hbm": {"algorithmic_bytes": sb["total"],
+                     "achieved_GBs": round(sb["total"] / (ms * 1e-3) / 1e9, 1),
+                     "frac_of_peak": round(sb["total"] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
+        "kernels_ms_per_step": {n: round(v["ms_per_step"], 4) for n, v in g["kernels"].items()},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        log("timing the fp64 oracle on the host (cpu_baseline)")
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_sample_layers)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -190,6 +190,24 @@ dsi_status dsi_kv_import(dsi_kv* kv, int32_t window, int32_t layer, int32_t len,
 /* Set a window's length directly (after dsi_kv_import).  Stream-ordered. */
 dsi_status dsi_kv_set_length(dsi_kv* kv, int32_t window, int32_t len);
 
+/* Diagnostics: kernel classes of one verification step. */
+enum {
+  DSI_K_QKV = 1,     /* fused QKV projection + RoPE + KV append (one per layer) */
+  DSI_K_ATTN = 2,    /* window attention + chunk combine (two launches per layer) */
+  DSI_K_OPROJ = 3,   /* output projection + residual */
+  DSI_K_GATEUP = 4,  /* gate/up projection + SwiGLU */
+  DSI_K_DOWN = 5,    /* down projection + residual */
+  DSI_K_HEAD = 6,    /* final RMSNorm pack + LM head */
+  DSI_K_VERIFY = 7   /* accept/reject kernels */
+};
+
+/* Record a HIP event pair on the model's stream around every launch of one
+ * kernel class until dsi_profile_end, which synchronises the stream and
+ * returns the number of timed launches and their summed duration.  Adds a
+ * little host and stream overhead; not for the timed path. */
+dsi_status dsi_profile_begin(dsi_model* m, int32_t kernel_class);
+dsi_status dsi_profile_end(dsi_model* m, int32_t* launches, double* total_ms);
+
 /* Thread-local description of the last error. */
 const char* dsi_last_error(void);
 

@@ -1,5 +1,6 @@
 // Causal window-over-prefix attention with grouped KV heads, split over key
-// chunks, plus the log-sum-exp combine of the chunk partials.
+// chunks (one workgroup of eight waves per chunk), plus the log-sum-exp
+// combine of the chunk partials.
 //
 // Row i of window b (position L_b + i) attends to keys [0, L_b + i]: the
 // cached prefix and the window rows before it (the k+1 prompts of one
@@ -24,12 +25,13 @@ namespace dsi {
 namespace {
 
 template <int KVB, int HD>
-__global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
+__global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
+  constexpr int NWV = kAttnWaves;
   constexpr int DS = HD / 32;
   constexpr int DT = HD / 16;
-  __shared__ float sm[4][16];
-  __shared__ float sl[4][16];
-  __shared__ f32x4 so[4][DT][64];
+  __shared__ float sm[NWV][16];
+  __shared__ float sl[NWV][16];
+  __shared__ f32x4 so[NWV][DT][64];
 
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
@@ -88,26 +90,47 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   const int r16 = lane & 15;
   const int kgrp = (lane >> 4) * 8;
 
-  for (int p0 = c0 + 32 * w; p0 < c1; p0 += 128) {
-    f32x4 st[2];
+  for (int p0 = c0 + 32 * w; p0 < c1; p0 += 32 * NWV) {
+    // issue every K and V load of this 32-key step before any math
+    u32x4 kb16[2][DS], vb16[DT];
+    F8 kf32[2][DS], vf32[DT];
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
-      st[t] = f32x4{0.f, 0.f, 0.f, 0.f};
       const int key = p0 + (r16 >> 2) * 8 + t * 4 + (r16 & 3);
 #pragma unroll
       for (int ds = 0; ds < DS; ++ds) {
         const size_t kidx = kbase + (size_t)key * HD + ds * 32 + kgrp;
         if (KVB) {
-          const u32x4 kv = *(const u32x4*)((const uint16_t*)a.kc + kidx);
-          const bf16x8 kb = as_bf16x8(kv);
+          kb16[t][ds] = *(const u32x4*)((const uint16_t*)a.kc + kidx);
+        } else {
+          kf32[t][ds].a = *(const float4*)((const float*)a.kc + kidx);
+          kf32[t][ds].b = *(const float4*)((const float*)a.kc + kidx + 4);
+        }
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < DT; ++t) {
+      const size_t vidx = vbase + (size_t)(t * 16 + r16) * a.maxlen + p0 + kgrp;
+      if (KVB) {
+        vb16[t] = *(const u32x4*)((const uint16_t*)a.vc + vidx);
+      } else {
+        vf32[t].a = *(const float4*)((const float*)a.vc + vidx);
+        vf32[t].b = *(const float4*)((const float*)a.vc + vidx + 4);
+      }
+    }
+    f32x4 st[2];
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      st[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ds = 0; ds < DS; ++ds) {
+        if (KVB) {
+          const bf16x8 kb = as_bf16x8(kb16[t][ds]);
           st[t] = mfma_bf16(kb, qh[ds], st[t]);
           st[t] = mfma_bf16(kb, ql[ds], st[t]);
         } else {
-          F8 kf;
-          kf.a = *(const float4*)((const float*)a.kc + kidx);
-          kf.b = *(const float4*)((const float*)a.kc + kidx + 4);
 #pragma unroll
-          for (int e = 0; e < 8; ++e) st[t] = mfma_f32(f8_get(kf, e), f8_get(qf[ds], e), st[t]);
+          for (int e = 0; e < 8; ++e) st[t] = mfma_f32(f8_get(kf32[t][ds], e), f8_get(qf[ds], e), st[t]);
         }
       }
     }
@@ -152,25 +175,19 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
       }
 #pragma unroll
       for (int t = 0; t < DT; ++t) {
-        const size_t vidx = vbase + (size_t)(t * 16 + r16) * a.maxlen + p0 + kgrp;
-        const bf16x8 vv = as_bf16x8(*(const u32x4*)((const uint16_t*)a.vc + vidx));
+        const bf16x8 vv = as_bf16x8(vb16[t]);
         o[t] = mfma_bf16(vv, ph, o[t]);
         o[t] = mfma_bf16(vv, pl, o[t]);
       }
     } else {
 #pragma unroll
-      for (int t = 0; t < DT; ++t) {
-        const size_t vidx = vbase + (size_t)(t * 16 + r16) * a.maxlen + p0 + kgrp;
-        F8 vf;
-        vf.a = *(const float4*)((const float*)a.vc + vidx);
-        vf.b = *(const float4*)((const float*)a.vc + vidx + 4);
+      for (int t = 0; t < DT; ++t)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) o[t] = mfma_f32(f8_get(vf, e), pv[e], o[t]);
-      }
+        for (int e = 0; e < 8; ++e) o[t] = mfma_f32(f8_get(vf32[t], e), pv[e], o[t]);
     }
   }
 
-  // combine the four waves of this workgroup
+  // combine the waves of this workgroup into one partial (m, l, O)
   lrun += __shfl_xor(lrun, 16);
   lrun += __shfl_xor(lrun, 32);
   if (lane < 16) {
@@ -180,64 +197,97 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
 #pragma unroll
   for (int t = 0; t < DT; ++t) so[w][t][lane] = o[t];
   __syncthreads();
-  const size_t zyc = ((size_t)z * a.n_qtiles + y) * a.n_chunks + c;
-  for (int it = threadIdx.x; it < DT * 64; it += 256) {
+  const size_t zy = (size_t)z * a.n_qtiles + y;
+  const size_t zyc = zy * a.n_chunks + c;
+  for (int it = threadIdx.x; it < DT * 64; it += NWV * 64) {
     const int t = it >> 6, l = it & 63, q = l & 15;
-    float M = fmaxf(fmaxf(sm[0][q], sm[1][q]), fmaxf(sm[2][q], sm[3][q]));
+    float M = sm[0][q];
+#pragma unroll
+    for (int ww = 1; ww < NWV; ++ww) M = fmaxf(M, sm[ww][q]);
     const float b = (M == -INFINITY) ? 0.f : M;
     f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int ww = 0; ww < 4; ++ww) acc += so[ww][t][l] * expf(sm[ww][q] - b);
+    for (int ww = 0; ww < NWV; ++ww) acc += so[ww][t][l] * expf(sm[ww][q] - b);
     float* dst = a.part_o + (zyc * 16 + q) * HD + t * 16 + (l >> 4) * 4;
     *(float4*)dst = float4{acc[0], acc[1], acc[2], acc[3]};
   }
   if (threadIdx.x < 16) {
     const int q = threadIdx.x;
-    float M = fmaxf(fmaxf(sm[0][q], sm[1][q]), fmaxf(sm[2][q], sm[3][q]));
+    float M = sm[0][q];
+#pragma unroll
+    for (int ww = 1; ww < NWV; ++ww) M = fmaxf(M, sm[ww][q]);
     const float b = (M == -INFINITY) ? 0.f : M;
     float L = 0.f;
 #pragma unroll
-    for (int ww = 0; ww < 4; ++ww) L += sl[ww][q] * expf(sm[ww][q] - b);
+    for (int ww = 0; ww < NWV; ++ww) L += sl[ww][q] * expf(sm[ww][q] - b);
     a.part_ml[zyc * 16 + q] = make_float2(M, L);
   }
+
 }
 
+// Log-sum-exp combine of the chunk partials of one (window, KV head, query
+// tile): out = sum_c e^(m_c - M) O_c / sum_c e^(m_c - M) l_c, chunks in
+// order.  grid (HD/32 column slices, query tiles, windows*KV heads); the
+// per-query statistics are formed once in LDS and every thread's chunk loads
+// are independent, so they are in flight together.
 template <int HD>
-__global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a) {
-  const int y = blockIdx.x, z = blockIdx.y;
+__global__ __launch_bounds__(128) void k_attn_combine(AttnArgs a) {
+  __shared__ float cb[16], cinv[16];
+  const int xs = blockIdx.x, y = blockIdx.y, z = blockIdx.z;
   const int win = z / a.n_kv, kvh = z % a.n_kv;
   const int G = a.n_heads / a.n_kv;
   const int R = a.rows.rows_per_window;
   const size_t zy = (size_t)z * a.n_qtiles + y;
-  for (int it = threadIdx.x; it < 16 * HD; it += 256) {
-    const int q = it / HD, d = it % HD;
-    const int qi = y * 16 + q;
-    if (qi >= G * R) continue;
+  const float2* ml = a.part_ml + zy * a.n_chunks * 16;
+  if (threadIdx.x < 16) {
+    const int q = threadIdx.x;
     float M = -INFINITY;
-    for (int c = 0; c < a.n_chunks; ++c) M = fmaxf(M, a.part_ml[(zy * a.n_chunks + c) * 16 + q].x);
-    float L = 0.f, O = 0.f;
+#pragma unroll 8
+    for (int c = 0; c < a.n_chunks; ++c) M = fmaxf(M, ml[c * 16 + q].x);
+    const float b = (M == -INFINITY) ? 0.f : M;
+    float L = 0.f;
+#pragma unroll 8
     for (int c = 0; c < a.n_chunks; ++c) {
-      const float2 ml = a.part_ml[(zy * a.n_chunks + c) * 16 + q];
-      if (ml.x == -INFINITY) continue;
-      const float f = expf(ml.x - M);
-      L += ml.y * f;
-      O += a.part_o[((zy * a.n_chunks + c) * 16 + q) * HD + d] * f;
+      const float2 v = ml[c * 16 + q];
+      L += v.y * expf(v.x - b);
     }
-    const int gh = qi / R, ri = qi % R;
-    const int m = win * R + ri;
-    const int head = kvh * G + gh;
-    pack_store(a.out, a.wtype, m, head * HD + d, O / L);
+    cb[q] = b;
+    cinv[q] = 1.0f / L;
   }
+  __syncthreads();
+  // 128 threads: 16 queries x 8 float4 columns = 32 columns of this slice
+  const int q = threadIdx.x >> 3;
+  const int d = xs * 32 + (threadIdx.x & 7) * 4;
+  const int qi = y * 16 + q;
+  if (qi >= G * R) return;
+  const float b = cb[q];
+  float4 acc = float4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 8
+  for (int c = 0; c < a.n_chunks; ++c) {
+    const float f = expf(ml[c * 16 + q].x - b);
+    const float4 v = *(const float4*)(a.part_o + ((zy * a.n_chunks + c) * 16 + q) * HD + d);
+    acc.x += v.x * f;
+    acc.y += v.y * f;
+    acc.z += v.z * f;
+    acc.w += v.w * f;
+  }
+  const float inv = cinv[q];
+  const int m = win * R + qi % R;
+  const int col = (kvh * G + qi / R) * HD + d;
+  pack_store(a.out, a.wtype, m, col + 0, acc.x * inv);
+  pack_store(a.out, a.wtype, m, col + 1, acc.y * inv);
+  pack_store(a.out, a.wtype, m, col + 2, acc.z * inv);
+  pack_store(a.out, a.wtype, m, col + 3, acc.w * inv);
 }
 
 template <int KVB, int HD>
 hipError_t launch_hd(const AttnArgs& a, hipStream_t s) {
   dim3 g1(a.n_chunks, a.n_qtiles, a.n_windows * a.n_kv);
-  hipLaunchKernelGGL((k_attn<KVB, HD>), g1, dim3(256), 0, s, a);
+  hipLaunchKernelGGL((k_attn<KVB, HD>), g1, dim3(kAttnWaves * 64), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  dim3 g2(a.n_qtiles, a.n_windows * a.n_kv);
-  hipLaunchKernelGGL((k_attn_combine<HD>), g2, dim3(256), 0, s, a);
+  dim3 g2(HD / 32, a.n_qtiles, a.n_windows * a.n_kv);
+  hipLaunchKernelGGL((k_attn_combine<HD>), g2, dim3(128), 0, s, a);
   return hipGetLastError();
 }
 

@@ -69,6 +69,29 @@ __device__ __forceinline__ void pack_store(const PackRef& p, int wtype, int m, i
   }
 }
 
+// store 8 consecutive features f0..f0+7 (f0 % 8 == 0) of token m: one
+// 16-byte store per half for bf16 packs, two for fp32 packs
+__device__ __forceinline__ void pack_store8(const PackRef& p, int wtype, int m, int f0, const float* v) {
+  const size_t idx = pack_index(p.Kb, m, f0);
+  if (wtype == W_BF16) {
+    uint16_t hi[8], lo[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) split_bf16(v[e], hi[e], lo[e]);
+    u32x4 h, l;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      h[e] = (uint32_t)hi[2 * e] | ((uint32_t)hi[2 * e + 1] << 16);
+      l[e] = (uint32_t)lo[2 * e] | ((uint32_t)lo[2 * e + 1] << 16);
+    }
+    *(u32x4*)((uint16_t*)p.hi + idx) = h;
+    *(u32x4*)((uint16_t*)p.lo + idx) = l;
+  } else {
+    float* d = (float*)p.hi + idx;
+    *(float4*)d = float4{v[0], v[1], v[2], v[3]};
+    *(float4*)(d + 4) = float4{v[4], v[5], v[6], v[7]};
+  }
+}
+
 __device__ __forceinline__ float silu_f(float x) { return x / (1.0f + __expf(-x)); }
 
 }  // namespace dsi

@@ -50,11 +50,56 @@ __global__ void k_prepack(const T* __restrict__ src, int N, int K, T* __restrict
   }
 }
 
-__device__ __forceinline__ float load_w_elem(const void* p, int wtype, size_t i) {
-  return wtype == W_BF16 ? bf_bits2f(((const uint16_t*)p)[i]) : ((const float*)p)[i];
+// Row-wise RMSNorm into a GEMM pack.  One workgroup per token row; each
+// thread owns groups of 8 consecutive features (two 16-byte loads, one
+// 16-byte store per pack half), kept in registers between the two passes.
+constexpr int kNormGroups = 4;   // d_model <= 256 threads * 8 * 4 = 8192
+
+__device__ __forceinline__ void load8(const void* p, int wtype, size_t i, float* v) {
+  if (wtype == W_BF16) {
+    const u32x4 r = *(const u32x4*)((const uint16_t*)p + i);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      v[2 * e] = __uint_as_float(r[e] << 16);
+      v[2 * e + 1] = __uint_as_float(r[e] & 0xFFFF0000u);
+    }
+  } else {
+    const float4 a = *(const float4*)((const float*)p + i);
+    const float4 b = *(const float4*)((const float*)p + i + 4);
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+  }
 }
 
-// one workgroup per token row
+__device__ __forceinline__ void norm_row(float (&v)[kNormGroups][8], int d, int m, const float* gain,
+                                         float eps, int wtype, const PackRef& pack, float* sh) {
+  const int ng = d >> 3;
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < kNormGroups; ++i) {
+    const int g = threadIdx.x + 256 * i;
+    if (g < ng) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ss += v[i][e] * v[i][e];
+    }
+  }
+  const float tot = block_sum_256(ss, sh);
+  const float rs = 1.0f / sqrtf(tot / (float)d + eps);
+#pragma unroll
+  for (int i = 0; i < kNormGroups; ++i) {
+    const int g = threadIdx.x + 256 * i;
+    if (g < ng) {
+      const float4 g0 = *(const float4*)(gain + 8 * g);
+      const float4 g1 = *(const float4*)(gain + 8 * g + 4);
+      const float gg[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
+      float y[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) y[e] = v[i][e] * rs * gg[e];
+      pack_store8(pack, wtype, m, 8 * g, y);
+    }
+  }
+}
+
 __global__ __launch_bounds__(256) void k_embed_norm(EmbedArgs a) {
   __shared__ float sh[4];
   const int m = blockIdx.x;
@@ -63,28 +108,33 @@ __global__ __launch_bounds__(256) void k_embed_norm(EmbedArgs a) {
     if (threadIdx.x == 0) atomicOr(a.err, 1);
     tok = 0;
   }
-  float ss = 0.f;
-  for (int c = threadIdx.x; c < a.d; c += 256) {
-    const float v = load_w_elem(a.E, a.wtype, (size_t)tok * a.d + c);
-    a.x[(size_t)m * a.d + c] = v;
-    if (a.hidden0) a.hidden0[(size_t)m * a.d + c] = v;
-    ss += v * v;
+  float v[kNormGroups][8];
+  const int ng = a.d >> 3;
+#pragma unroll
+  for (int i = 0; i < kNormGroups; ++i) {
+    const int g = threadIdx.x + 256 * i;
+    if (g < ng) {
+      load8(a.E, a.wtype, (size_t)tok * a.d + 8 * g, v[i]);
+      float* xr = a.x + (size_t)m * a.d + 8 * g;
+      *(float4*)xr = float4{v[i][0], v[i][1], v[i][2], v[i][3]};
+      *(float4*)(xr + 4) = float4{v[i][4], v[i][5], v[i][6], v[i][7]};
+      if (a.hidden0) {
+        float* hr = a.hidden0 + (size_t)m * a.d + 8 * g;
+        *(float4*)hr = float4{v[i][0], v[i][1], v[i][2], v[i][3]};
+        *(float4*)(hr + 4) = float4{v[i][4], v[i][5], v[i][6], v[i][7]};
+      }
+    }
   }
-  const float tot = block_sum_256(ss, sh);
-  const float rs = 1.0f / sqrtf(tot / (float)a.d + a.eps);
-  for (int c = threadIdx.x; c < a.d; c += 256) {
-    const float v = load_w_elem(a.E, a.wtype, (size_t)tok * a.d + c);
-    pack_store(a.pack, a.wtype, m, c, v * rs * a.gain[c]);
-  }
+  norm_row(v, a.d, m, a.gain, a.eps, a.wtype, a.pack, sh);
   // rotary table of this row's position: angle = pos * base^(-2j/hd), fp64
   const int R = a.rows.rows_per_window;
   const int pos = a.rows.lens[a.rows.window0 + m / R] + (m % R);
   const int half = a.hd >> 1;
   for (int j = threadIdx.x; j < half; j += 256) {
     const double inv = exp2(-2.0 * (double)j / (double)a.hd * a.log2_base);
-    double s, c;
-    sincos((double)pos * inv, &s, &c);
-    a.rope[(size_t)m * half + j] = make_float2((float)c, (float)s);
+    double sn, cs;
+    sincos((double)pos * inv, &sn, &cs);
+    a.rope[(size_t)m * half + j] = make_float2((float)cs, (float)sn);
   }
 }
 
@@ -93,16 +143,21 @@ __global__ __launch_bounds__(256) void k_rmsnorm_pack(const float* __restrict__ 
                                                        int wtype, PackRef pack, float* copy_out) {
   __shared__ float sh[4];
   const int m = blockIdx.x;
-  const float* xr = x + (size_t)m * d;
-  float ss = 0.f;
-  for (int c = threadIdx.x; c < d; c += 256) {
-    const float v = xr[c];
-    ss += v * v;
-    if (copy_out) copy_out[(size_t)m * d + c] = v;
+  float v[kNormGroups][8];
+  const int ng = d >> 3;
+#pragma unroll
+  for (int i = 0; i < kNormGroups; ++i) {
+    const int g = threadIdx.x + 256 * i;
+    if (g < ng) {
+      load8(x, W_F32, (size_t)m * d + 8 * g, v[i]);
+      if (copy_out) {
+        float* hr = copy_out + (size_t)m * d + 8 * g;
+        *(float4*)hr = float4{v[i][0], v[i][1], v[i][2], v[i][3]};
+        *(float4*)(hr + 4) = float4{v[i][4], v[i][5], v[i][6], v[i][7]};
+      }
+    }
   }
-  const float tot = block_sum_256(ss, sh);
-  const float rs = 1.0f / sqrtf(tot / (float)d + eps);
-  for (int c = threadIdx.x; c < d; c += 256) pack_store(pack, wtype, m, c, xr[c] * rs * gain[c]);
+  norm_row(v, d, m, gain, eps, wtype, pack, sh);
 }
 
 __global__ void k_kv_rollback(int* lens, int window, int new_len, int* err) {

@@ -20,9 +20,9 @@ namespace dsi {
 
 namespace {
 
-template <int WT>
+template <int WT, int EPI>
 __device__ __forceinline__ void epilogue(const EpiArgs& e, int nb, int r0, int m, f32x4 s) {
-  switch (e.kind) {
+  switch (EPI) {
     case EPI_STORE: {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
@@ -100,17 +100,45 @@ __device__ __forceinline__ void epilogue(const EpiArgs& e, int nb, int r0, int m
   }
 }
 
-template <int MT, int NBW, int NW, int U>
+// Sum the NW per-wave partial tiles in wave order (deterministic) and run the
+// epilogue on this workgroup's n-blocks.
+template <int WT, int EPI, int MT, int NBW, int NW>
+__device__ __forceinline__ void finish(const GemmArgs& a, const f32x4* red, int nb0) {
+  constexpr int ACC = NBW * MT;
+  for (int it = threadIdx.x; it < ACC * 64; it += NW * 64) {
+    const int l = it & 63, jm = it >> 6;
+    const int j = jm / MT, t = jm % MT;
+    f32x4 v = red[jm * 64 + l];
+    for (int ww = 1; ww < NW; ++ww) v += red[(ww * ACC + jm) * 64 + l];
+    const int nb = nb0 + j, m = t * 16 + (l & 15);
+    if (nb < a.Nb && m < a.M) epilogue<WT, EPI>(a.epi, nb, (l >> 4) * 4, m, v);
+  }
+}
+
+// workgroup -> its n-blocks; wave -> a contiguous k-block range
+struct Work {
+  int nb0, nbv, kb_beg, kb_end;
+};
+template <int NBW, int NW>
+__device__ __forceinline__ Work work_of(const GemmArgs& a) {
+  Work w;
+  w.nb0 = blockIdx.x * NBW;
+  w.nbv = min(NBW, a.Nb - w.nb0);
+  const int per = (a.Kb + NW - 1) / NW;
+  const int wave = threadIdx.x >> 6;
+  w.kb_beg = min(a.Kb, wave * per);
+  w.kb_end = min(a.Kb, w.kb_beg + per);
+  return w;
+}
+
+template <int MT, int NBW, int NW, int U, int EPI>
 __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(GemmArgs a) {
   constexpr int ACC = NBW * MT;
   __shared__ f32x4 red[NW * ACC * 64];
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
-  const int nb0 = blockIdx.x * NBW;
-  const int nbv = min(NBW, a.Nb - nb0);
-  const int per = (a.Kb + NW - 1) / NW;
-  const int kb_beg = min(a.Kb, w * per);
-  const int kb_end = min(a.Kb, kb_beg + per);
+  const Work wk = work_of<NBW, NW>(a);
+  const int nb0 = wk.nb0, nbv = wk.nbv, kb_beg = wk.kb_beg, kb_end = wk.kb_end;
   const u32x4* __restrict__ W = (const u32x4*)a.W;
   const u32x4* __restrict__ Xh = (const u32x4*)a.Xhi;
   const u32x4* __restrict__ Xl = (const u32x4*)a.Xlo;
@@ -167,27 +195,17 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(GemmArgs a) {
 #pragma unroll
     for (int t = 0; t < MT; ++t) red[((w * NBW + j) * MT + t) * 64 + lane] = acc[j][t];
   __syncthreads();
-  for (int it = threadIdx.x; it < ACC * 64; it += NW * 64) {
-    const int l = it & 63, jm = it >> 6;
-    const int j = jm / MT, t = jm % MT;
-    f32x4 s = red[jm * 64 + l];
-    for (int ww = 1; ww < NW; ++ww) s += red[(ww * ACC + jm) * 64 + l];
-    const int nb = nb0 + j, m = t * 16 + (l & 15);
-    if (nb < a.Nb && m < a.M) epilogue<W_BF16>(a.epi, nb, (l >> 4) * 4, m, s);
-  }
+  finish<W_BF16, EPI, MT, NBW, NW>(a, red, nb0);
 }
 
-template <int MT, int NBW, int NW>
+template <int MT, int NBW, int NW, int EPI>
 __global__ __launch_bounds__(NW * 64) void k_gemm_f32(GemmArgs a) {
   constexpr int ACC = NBW * MT;
   __shared__ f32x4 red[NW * ACC * 64];
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
-  const int nb0 = blockIdx.x * NBW;
-  const int nbv = min(NBW, a.Nb - nb0);
-  const int per = (a.Kb + NW - 1) / NW;
-  const int kb_beg = min(a.Kb, w * per);
-  const int kb_end = min(a.Kb, kb_beg + per);
+  const Work wk = work_of<NBW, NW>(a);
+  const int nb0 = wk.nb0, nbv = wk.nbv, kb_beg = wk.kb_beg, kb_end = wk.kb_end;
   const float4* __restrict__ W = (const float4*)a.W;
   const float4* __restrict__ X = (const float4*)a.Xhi;
 
@@ -227,50 +245,67 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_f32(GemmArgs a) {
 #pragma unroll
     for (int t = 0; t < MT; ++t) red[((w * NBW + j) * MT + t) * 64 + lane] = acc[j][t];
   __syncthreads();
-  for (int it = threadIdx.x; it < ACC * 64; it += NW * 64) {
-    const int l = it & 63, jm = it >> 6;
-    const int j = jm / MT, t = jm % MT;
-    f32x4 s = red[jm * 64 + l];
-    for (int ww = 1; ww < NW; ++ww) s += red[(ww * ACC + jm) * 64 + l];
-    const int nb = nb0 + j, m = t * 16 + (l & 15);
-    if (nb < a.Nb && m < a.M) epilogue<W_F32>(a.epi, nb, (l >> 4) * 4, m, s);
-  }
+  finish<W_F32, EPI, MT, NBW, NW>(a, red, nb0);
 }
 
-template <int MT>
-hipError_t launch_bf16(const GemmArgs& a, hipStream_t s) {
-  constexpr int NBW = 2, NW = 8, U = 4;
+// Grid shaping.  Every n-block belongs to exactly one workgroup, whose waves
+// split K and reduce through LDS (no cross-workgroup traffic: on this part a
+// device-scope handoff costs an L2 write-back and invalidate).  Narrow
+// outputs (QKV, O, down: a few hundred n-blocks) use 16-wave workgroups so
+// one workgroup per CU keeps enough loads in flight; wide ones use 8 waves,
+// and two n-blocks per workgroup once there are thousands of n-blocks.
+template <int MT, int EPI, int NBW, int NW>
+hipError_t launch_bf16_cfg(const GemmArgs& a, hipStream_t s) {
+  constexpr int U = 4;
   const int grid = (a.Nb + NBW - 1) / NBW;
-  hipLaunchKernelGGL((k_gemm_bf16<MT, NBW, NW, U>), dim3(grid), dim3(NW * 64), 0, s, a);
+  hipLaunchKernelGGL((k_gemm_bf16<MT, NBW, NW, U, EPI>), dim3(grid), dim3(NW * 64), 0, s, a);
   return hipGetLastError();
 }
 
-template <int MT>
+template <int MT, int EPI>
+hipError_t launch_bf16(const GemmArgs& a, hipStream_t s) {
+  if (a.Nb <= 768) return launch_bf16_cfg<MT, EPI, 1, 16>(a, s);
+  if (a.Nb <= 4096) return launch_bf16_cfg<MT, EPI, 1, 8>(a, s);
+  return launch_bf16_cfg<MT, EPI, 2, 8>(a, s);
+}
+
+template <int MT, int EPI>
 hipError_t launch_f32(const GemmArgs& a, hipStream_t s) {
   constexpr int NBW = 1, NW = 4;
   const int grid = (a.Nb + NBW - 1) / NBW;
-  hipLaunchKernelGGL((k_gemm_f32<MT, NBW, NW>), dim3(grid), dim3(NW * 64), 0, s, a);
+  hipLaunchKernelGGL((k_gemm_f32<MT, NBW, NW, EPI>), dim3(grid), dim3(NW * 64), 0, s, a);
   return hipGetLastError();
+}
+
+template <int EPI>
+hipError_t launch_epi(int wtype, int mt, const GemmArgs& a, hipStream_t s) {
+  if (wtype == W_BF16) {
+    switch (mt) {
+      case 1: return launch_bf16<1, EPI>(a, s);
+      case 2: return launch_bf16<2, EPI>(a, s);
+      case 3: return launch_bf16<3, EPI>(a, s);
+      case 4: return launch_bf16<4, EPI>(a, s);
+    }
+  } else {
+    switch (mt) {
+      case 1: return launch_f32<1, EPI>(a, s);
+      case 2: return launch_f32<2, EPI>(a, s);
+      case 3: return launch_f32<3, EPI>(a, s);
+      case 4: return launch_f32<4, EPI>(a, s);
+    }
+  }
+  return hipErrorInvalidValue;
 }
 
 }  // namespace
 
 hipError_t launch_gemm(int wtype, int mt, const GemmArgs& a, hipStream_t s) {
   if (a.Nb <= 0 || a.M <= 0) return hipSuccess;
-  if (wtype == W_BF16) {
-    switch (mt) {
-      case 1: return launch_bf16<1>(a, s);
-      case 2: return launch_bf16<2>(a, s);
-      case 3: return launch_bf16<3>(a, s);
-      case 4: return launch_bf16<4>(a, s);
-    }
-  } else {
-    switch (mt) {
-      case 1: return launch_f32<1>(a, s);
-      case 2: return launch_f32<2>(a, s);
-      case 3: return launch_f32<3>(a, s);
-      case 4: return launch_f32<4>(a, s);
-    }
+  switch (a.epi.kind) {
+    case EPI_STORE: return launch_epi<EPI_STORE>(wtype, mt, a, s);
+    case EPI_RESID: return launch_epi<EPI_RESID>(wtype, mt, a, s);
+    case EPI_QKV: return launch_epi<EPI_QKV>(wtype, mt, a, s);
+    case EPI_SILU: return launch_epi<EPI_SILU>(wtype, mt, a, s);
   }
   return hipErrorInvalidValue;
 }

@@ -133,6 +133,8 @@ struct AttnArgs {
   PackRef out;          // O-projection input pack
   int wtype;
 };
+constexpr int kAttnWaves = 8;                       // waves per attention workgroup
+constexpr int kAttnChunkQuantum = kAttnWaves * 32;  // keys per workgroup step
 hipError_t launch_attention(int kv_bf16, int hd, const AttnArgs& a, hipStream_t s);
 
 // verification (verify.hip)

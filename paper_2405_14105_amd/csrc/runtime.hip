@@ -105,6 +105,10 @@ struct dsi_model {
   int* err = nullptr;
   DevBuf attn_o, attn_ml;
   int live_kv = 0;
+  // diagnostics: event pairs around one kernel class
+  int prof_class = 0;
+  std::vector<hipEvent_t> prof_ev;
+  size_t prof_used = 0;
 };
 
 struct dsi_kv {
@@ -161,6 +165,27 @@ PackRef make_pack(dsi_model* m, int Kb, dsi_status* st) {
   return p;
 }
 
+// event pair around the launches of one kernel class (diagnostics only)
+struct Prof {
+  dsi_model* m;
+  int idx = -1;
+  Prof(dsi_model* mm, int cls) : m(mm) {
+    if (m->prof_class != cls) return;
+    if (m->prof_used + 2 > m->prof_ev.size()) {
+      hipEvent_t a, b;
+      if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) return;
+      m->prof_ev.push_back(a);
+      m->prof_ev.push_back(b);
+    }
+    idx = (int)m->prof_used;
+    m->prof_used += 2;
+    hipEventRecord(m->prof_ev[idx], m->stream);
+  }
+  ~Prof() {
+    if (idx >= 0) hipEventRecord(m->prof_ev[idx + 1], m->stream);
+  }
+};
+
 // ------------------------------------------------------------- forward plan
 //
 // One target forward over M = B * R rows: R consecutive rows of each of the
@@ -204,9 +229,9 @@ dsi_status run_forward(dsi_model* m, dsi_kv* kv, int window0, int B, int R, cons
   const int G = m->hq / m->hkv;
   const int n_qtiles = cdiv(G * R, 16);
   const int zq = B * m->hkv * n_qtiles;
-  const int want = std::max(1, cdiv(1024, m->hkv * n_qtiles));
-  int chunk = (int)round_up((size_t)cdiv(kv->max_len, want), 128);
-  chunk = std::min(std::max(chunk, 128), 8192);
+  const int want = std::max(1, cdiv(512, m->hkv * n_qtiles));
+  int chunk = (int)round_up((size_t)cdiv(kv->max_len, want), kAttnChunkQuantum);
+  chunk = std::min(std::max(chunk, kAttnChunkQuantum), 16384);
   const int n_chunks = (int)((kmax + chunk - 1) / chunk);
   const size_t nparts = (size_t)zq * n_chunks * 16;
   DSI_TRY(ensure(m->attn_o, nparts * m->hd * sizeof(float)));
@@ -233,7 +258,10 @@ dsi_status run_forward(dsi_model* m, dsi_kv* kv, int window0, int B, int R, cons
     g.epi.maxlen = kv->maxlen_pad;
     g.epi.rope = m->rope;
     g.epi.rows = rows;
-    HIP_TRY(launch_gemm(m->wtype, mt, g, s));
+    {
+      Prof p(m, DSI_K_QKV);
+      HIP_TRY(launch_gemm(m->wtype, mt, g, s));
+    }
 
     AttnArgs aa{};
     aa.q = m->qbuf;
@@ -252,8 +280,10 @@ dsi_status run_forward(dsi_model* m, dsi_kv* kv, int window0, int B, int R, cons
     aa.part_ml = (float2*)m->attn_ml.p;
     aa.out = m->pk_q;
     aa.wtype = m->wtype;
-    // windows beyond window0 are addressed through rows.window0 + win
-    HIP_TRY(launch_attention(m->kvb, m->hd, aa, s));
+    {
+      Prof p(m, DSI_K_ATTN);
+      HIP_TRY(launch_attention(m->kvb, m->hd, aa, s));
+    }
 
     // O projection + residual
     GemmArgs go{};
@@ -267,7 +297,10 @@ dsi_status run_forward(dsi_model* m, dsi_kv* kv, int window0, int B, int R, cons
     go.epi.out = m->x;
     go.epi.ld = m->d;
     go.epi.n_valid = m->d;
-    HIP_TRY(launch_gemm(m->wtype, mt, go, s));
+    {
+      Prof p(m, DSI_K_OPROJ);
+      HIP_TRY(launch_gemm(m->wtype, mt, go, s));
+    }
 
     HIP_TRY(launch_rmsnorm_pack(m->x, M, m->d, lw.ffn_norm, m->cfg.rms_eps, m->wtype, m->pk_d,
                                 nullptr, s));
@@ -282,7 +315,10 @@ dsi_status run_forward(dsi_model* m, dsi_kv* kv, int window0, int B, int R, cons
     gu.epi.kind = EPI_SILU;
     gu.epi.pack = m->pk_ff;
     gu.epi.ff = m->ff;
-    HIP_TRY(launch_gemm(m->wtype, mt, gu, s));
+    {
+      Prof p(m, DSI_K_GATEUP);
+      HIP_TRY(launch_gemm(m->wtype, mt, gu, s));
+    }
     // down + residual
     GemmArgs gd{};
     gd.M = M;
@@ -295,7 +331,10 @@ dsi_status run_forward(dsi_model* m, dsi_kv* kv, int window0, int B, int R, cons
     gd.epi.out = m->x;
     gd.epi.ld = m->d;
     gd.epi.n_valid = m->d;
-    HIP_TRY(launch_gemm(m->wtype, mt, gd, s));
+    {
+      Prof p(m, DSI_K_DOWN);
+      HIP_TRY(launch_gemm(m->wtype, mt, gd, s));
+    }
 
     if (l + 1 < m->L) {
       HIP_TRY(launch_rmsnorm_pack(m->x, M, m->d, m->layers[l + 1].attn_norm, m->cfg.rms_eps,
@@ -317,6 +356,7 @@ dsi_status run_forward(dsi_model* m, dsi_kv* kv, int window0, int B, int R, cons
   gh.epi.out = logits;
   gh.epi.ld = m->V;
   gh.epi.n_valid = m->V;
+  Prof ph(m, DSI_K_HEAD);
   if (head_last_only) {
     HIP_TRY(launch_rmsnorm_pack(m->x + (size_t)(M - 1) * m->d, 1, m->d, m->final_norm,
                                 m->cfg.rms_eps, m->wtype, m->pk_d, nullptr, s));
@@ -383,6 +423,7 @@ dsi_status dsi_model_create(const dsi_config* cfg, void* stream, dsi_model** out
   if (c.n_layers < 1 || c.d_model < 32 || c.d_model % 32 || c.n_heads < 1 || c.n_kv_heads < 1 ||
       c.n_heads % c.n_kv_heads || c.d_ff < 1 || c.vocab < 1)
     return fail(DSI_EINVAL, "invalid shape (d_model must be a multiple of 32)");
+  if (c.d_model > 8192) return fail(DSI_EINVAL, "d_model must be at most 8192");
   if (c.head_dim != 32 && c.head_dim != 64 && c.head_dim != 96 && c.head_dim != 128)
     return fail(DSI_EINVAL, "head_dim must be 32, 64, 96 or 128");
   if ((c.wdtype != DSI_F32 && c.wdtype != DSI_BF16) || (c.kvdtype != DSI_F32 && c.kvdtype != DSI_BF16))
@@ -441,6 +482,7 @@ dsi_status dsi_model_create(const dsi_config* cfg, void* stream, dsi_model** out
   A((void**)&m->rope, (size_t)kMaxRows * (m->hd / 2) * sizeof(float2));
   A((void**)&m->logits, (size_t)kMaxRows * m->V * 4);
   A(&m->vws, verify_workspace_bytes(kMaxRows, kMaxRows, m->V));
+
   A((void**)&m->err, 64);
   if (st != DSI_OK) {
     free_list(m->allocs);
@@ -455,6 +497,7 @@ dsi_status dsi_model_destroy(dsi_model* m) {
   if (!m) return DSI_OK;
   if (m->live_kv) return fail(DSI_ESTATE, "destroy the model's KV caches first");
   hipStreamSynchronize(m->stream);
+  for (hipEvent_t e : m->prof_ev) hipEventDestroy(e);
   free_list(m->allocs);
   if (m->attn_o.p) hipFree(m->attn_o.p);
   if (m->attn_ml.p) hipFree(m->attn_ml.p);
@@ -631,7 +674,10 @@ dsi_status dsi_verify(dsi_model* m, dsi_kv* kv, const dsi_verify_args* a, int32_
   va.tok_out = d_next_token;
   va.err = m->err;
   verify_bind_workspace(va, m->vws, B * (k + 1), B, m->V);
-  HIP_TRY(launch_verify(va, m->stream));
+  {
+    Prof p(m, DSI_K_VERIFY);
+    HIP_TRY(launch_verify(va, m->stream));
+  }
   if (a->commit)
     for (int b = 0; b < B; ++b) kv->hi[a->window0 + b] += k + 1;
   return DSI_OK;
@@ -697,6 +743,31 @@ dsi_status dsi_kv_length(dsi_kv* kv, int32_t window, int32_t* len) {
   *len = h;
   kv->hi[window] = kv->lo[window] = h;
   return check_err_word(kv->m->err, kv->m->stream);
+}
+
+dsi_status dsi_profile_begin(dsi_model* m, int32_t kernel_class) {
+  if (!m) return fail(DSI_EINVAL, "null model");
+  if (kernel_class < DSI_K_QKV || kernel_class > DSI_K_VERIFY) return fail(DSI_EINVAL, "bad kernel class");
+  HIP_TRY(hipStreamSynchronize(m->stream));
+  m->prof_class = kernel_class;
+  m->prof_used = 0;
+  return DSI_OK;
+}
+
+dsi_status dsi_profile_end(dsi_model* m, int32_t* launches, double* total_ms) {
+  if (!m || !launches || !total_ms) return fail(DSI_EINVAL, "null argument");
+  HIP_TRY(hipStreamSynchronize(m->stream));
+  double tot = 0.0;
+  for (size_t i = 0; i + 1 < m->prof_used; i += 2) {
+    float ms = 0.f;
+    HIP_TRY(hipEventElapsedTime(&ms, m->prof_ev[i], m->prof_ev[i + 1]));
+    tot += ms;
+  }
+  *launches = (int32_t)(m->prof_used / 2);
+  *total_ms = tot;
+  m->prof_class = 0;
+  m->prof_used = 0;
+  return DSI_OK;
 }
 
 dsi_status dsi_sync(dsi_model* m) {

@@ -27,8 +27,9 @@ EXPORTED = (
     "dsi_model_create", "dsi_model_set_tensor", "dsi_model_destroy", "dsi_kv_create",
     "dsi_kv_destroy", "dsi_prefill", "dsi_verify", "dsi_accept", "dsi_kv_rollback",
     "dsi_kv_length", "dsi_sync", "dsi_kv_export", "dsi_kv_import", "dsi_kv_set_length",
-    "dsi_last_error",
+    "dsi_profile_begin", "dsi_profile_end", "dsi_last_error",
 )
+DSI_K_QKV, DSI_K_ATTN, DSI_K_OPROJ, DSI_K_GATEUP, DSI_K_DOWN, DSI_K_HEAD, DSI_K_VERIFY = range(1, 8)
 
 
 class DsiError(RuntimeError):
@@ -83,6 +84,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "dsi_kv_export": ([P, I32, I32, I32, P, P], I32),
         "dsi_kv_import": ([P, I32, I32, I32, P, P], I32),
         "dsi_kv_set_length": ([P, I32, I32], I32),
+        "dsi_profile_begin": ([P, I32], I32),
+        "dsi_profile_end": ([P, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_double)], I32),
         "dsi_last_error": ([], ctypes.c_char_p),
     }
     for name, (args, res) in sig.items():
@@ -179,6 +182,18 @@ def dsi_kv_import(kv: int, window: int, layer: int, length: int, d_k, d_v):
 
 def dsi_kv_set_length(kv: int, window: int, length: int):
     _check(load().dsi_kv_set_length(kv, window, length))
+
+
+def dsi_profile_begin(model: int, kernel_class: int):
+    _check(load().dsi_profile_begin(model, kernel_class))
+
+
+def dsi_profile_end(model: int):
+    """Returns (launches, total_ms)."""
+    n = ctypes.c_int32()
+    t = ctypes.c_double()
+    _check(load().dsi_profile_end(model, ctypes.byref(n), ctypes.byref(t)))
+    return n.value, t.value
 
 
 def dsi_last_error() -> str:

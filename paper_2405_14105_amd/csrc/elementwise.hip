@@ -138,7 +138,8 @@ __global__ __launch_bounds__(256) void k_embed_norm(EmbedArgs a) {
   }
 }
 
-__global__ __launch_bounds__(256) void k_rmsnorm_pack(const float* __restrict__ x, int d,
+__global__ __launch_bounds__(256) void k_rmsnorm_pack(float* __restrict__ x, const float* __restrict__ delta,
+                                                       int S, size_t dstride, int d,
                                                        const float* __restrict__ gain, float eps,
                                                        int wtype, PackRef pack, float* copy_out) {
   __shared__ float sh[4];
@@ -149,9 +150,21 @@ __global__ __launch_bounds__(256) void k_rmsnorm_pack(const float* __restrict__ 
   for (int i = 0; i < kNormGroups; ++i) {
     const int g = threadIdx.x + 256 * i;
     if (g < ng) {
-      load8(x, W_F32, (size_t)m * d + 8 * g, v[i]);
+      const size_t off = (size_t)m * d + 8 * g;
+      load8(x, W_F32, off, v[i]);
+      if (S > 0) {
+        for (int sp = 0; sp < S; ++sp) {
+          float p[8];
+          load8(delta + sp * dstride, W_F32, off, p);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[i][e] += p[e];
+        }
+        float* xr = x + off;
+        *(float4*)xr = float4{v[i][0], v[i][1], v[i][2], v[i][3]};
+        *(float4*)(xr + 4) = float4{v[i][4], v[i][5], v[i][6], v[i][7]};
+      }
       if (copy_out) {
-        float* hr = copy_out + (size_t)m * d + 8 * g;
+        float* hr = copy_out + off;
         *(float4*)hr = float4{v[i][0], v[i][1], v[i][2], v[i][3]};
         *(float4*)(hr + 4) = float4{v[i][4], v[i][5], v[i][6], v[i][7]};
       }
@@ -245,9 +258,11 @@ hipError_t launch_embed_norm(const EmbedArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_rmsnorm_pack(const float* x, int M, int d, const float* gain, float eps, int wtype,
-                               PackRef pack, float* copy_out, hipStream_t s) {
-  hipLaunchKernelGGL(k_rmsnorm_pack, dim3(M), dim3(256), 0, s, x, d, gain, eps, wtype, pack, copy_out);
+hipError_t launch_rmsnorm_pack(float* x, const float* delta, int S, size_t delta_stride, int M, int d,
+                               const float* gain, float eps, int wtype, PackRef pack, float* copy_out,
+                               hipStream_t s) {
+  hipLaunchKernelGGL(k_rmsnorm_pack, dim3(M), dim3(256), 0, s, x, delta, S, delta_stride, d, gain, eps,
+                     wtype, pack, copy_out);
   return hipGetLastError();
 }
 

@@ -14,6 +14,8 @@
 //    (deterministic, no float atomics) and handed to the epilogue;
 //  * weight loads for the next U k-blocks are issued before the MFMAs of the
 //    current ones so every wave keeps U*NBW KB in flight.
+#include <algorithm>
+
 #include "device_util.h"
 
 namespace dsi {
@@ -21,7 +23,7 @@ namespace dsi {
 namespace {
 
 template <int WT, int EPI>
-__device__ __forceinline__ void epilogue(const EpiArgs& e, int nb, int r0, int m, f32x4 s) {
+__device__ __forceinline__ void epilogue(const EpiArgs& e, int nb, int r0, int m, int split, f32x4 s) {
   switch (EPI) {
     case EPI_STORE: {
 #pragma unroll
@@ -31,11 +33,12 @@ __device__ __forceinline__ void epilogue(const EpiArgs& e, int nb, int r0, int m
       }
       break;
     }
-    case EPI_RESID: {
+    case EPI_PART: {
+      float* o = e.out + split * e.part_stride + (size_t)m * e.ld;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int n = nb * 16 + r0 + j;
-        if (n < e.n_valid) e.out[(size_t)m * e.ld + n] += s[j];
+        if (n < e.n_valid) o[n] = s[j];
       }
       break;
     }
@@ -103,7 +106,7 @@ __device__ __forceinline__ void epilogue(const EpiArgs& e, int nb, int r0, int m
 // Sum the NW per-wave partial tiles in wave order (deterministic) and run the
 // epilogue on this workgroup's n-blocks.
 template <int WT, int EPI, int MT, int NBW, int NW>
-__device__ __forceinline__ void finish(const GemmArgs& a, const f32x4* red, int nb0) {
+__device__ __forceinline__ void finish(const GemmArgs& a, const f32x4* red, int nb0, int split) {
   constexpr int ACC = NBW * MT;
   for (int it = threadIdx.x; it < ACC * 64; it += NW * 64) {
     const int l = it & 63, jm = it >> 6;
@@ -111,23 +114,27 @@ __device__ __forceinline__ void finish(const GemmArgs& a, const f32x4* red, int 
     f32x4 v = red[jm * 64 + l];
     for (int ww = 1; ww < NW; ++ww) v += red[(ww * ACC + jm) * 64 + l];
     const int nb = nb0 + j, m = t * 16 + (l & 15);
-    if (nb < a.Nb && m < a.M) epilogue<WT, EPI>(a.epi, nb, (l >> 4) * 4, m, v);
+    if (nb < a.Nb && m < a.M) epilogue<WT, EPI>(a.epi, nb, (l >> 4) * 4, m, split, v);
   }
 }
 
-// workgroup -> its n-blocks; wave -> a contiguous k-block range
+// workgroup -> (n-block group, K split); wave -> contiguous k-blocks of it
 struct Work {
-  int nb0, nbv, kb_beg, kb_end;
+  int nb0, nbv, split, kb_beg, kb_end;
 };
 template <int NBW, int NW>
 __device__ __forceinline__ Work work_of(const GemmArgs& a) {
   Work w;
-  w.nb0 = blockIdx.x * NBW;
+  const int g = blockIdx.x / a.S;
+  w.split = blockIdx.x % a.S;
+  w.nb0 = g * NBW;
   w.nbv = min(NBW, a.Nb - w.nb0);
-  const int per = (a.Kb + NW - 1) / NW;
+  const int k0 = (w.split * a.Kb) / a.S;
+  const int k1 = ((w.split + 1) * a.Kb) / a.S;
+  const int per = (k1 - k0 + NW - 1) / NW;
   const int wave = threadIdx.x >> 6;
-  w.kb_beg = min(a.Kb, wave * per);
-  w.kb_end = min(a.Kb, w.kb_beg + per);
+  w.kb_beg = min(k1, k0 + wave * per);
+  w.kb_end = min(k1, w.kb_beg + per);
   return w;
 }
 
@@ -195,7 +202,7 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(GemmArgs a) {
 #pragma unroll
     for (int t = 0; t < MT; ++t) red[((w * NBW + j) * MT + t) * 64 + lane] = acc[j][t];
   __syncthreads();
-  finish<W_BF16, EPI, MT, NBW, NW>(a, red, nb0);
+  finish<W_BF16, EPI, MT, NBW, NW>(a, red, nb0, wk.split);
 }
 
 template <int MT, int NBW, int NW, int EPI>
@@ -245,34 +252,43 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_f32(GemmArgs a) {
 #pragma unroll
     for (int t = 0; t < MT; ++t) red[((w * NBW + j) * MT + t) * 64 + lane] = acc[j][t];
   __syncthreads();
-  finish<W_F32, EPI, MT, NBW, NW>(a, red, nb0);
+  finish<W_F32, EPI, MT, NBW, NW>(a, red, nb0, wk.split);
 }
 
-// Grid shaping.  Every n-block belongs to exactly one workgroup, whose waves
-// split K and reduce through LDS (no cross-workgroup traffic: on this part a
-// device-scope handoff costs an L2 write-back and invalidate).  Narrow
-// outputs (QKV, O, down: a few hundred n-blocks) use 16-wave workgroups so
-// one workgroup per CU keeps enough loads in flight; wide ones use 8 waves,
-// and two n-blocks per workgroup once there are thousands of n-blocks.
-template <int MT, int EPI, int NBW, int NW>
-hipError_t launch_bf16_cfg(const GemmArgs& a, hipStream_t s) {
-  constexpr int U = 4;
-  const int grid = (a.Nb + NBW - 1) / NBW;
+// Grid shaping.  Each wave reuses every activation fragment it loads across
+// the NBW n-blocks of its workgroup (activation reads from L2, not the
+// weight stream, are what limit a one-n-block-per-wave GEMM); waves split K
+// inside the workgroup and reduce through LDS.  Narrow EPI_PART GEMMs (O and
+// down projections) also split K across S workgroups, each writing its own
+// partial buffer, so the grid still covers every CU without any
+// cross-workgroup synchronisation.
+template <int MT, int EPI, int NBW, int NW, int U>
+hipError_t launch_bf16_cfg(GemmArgs a, hipStream_t s) {
+  const int grid = ((a.Nb + NBW - 1) / NBW) * a.S;
   hipLaunchKernelGGL((k_gemm_bf16<MT, NBW, NW, U, EPI>), dim3(grid), dim3(NW * 64), 0, s, a);
   return hipGetLastError();
 }
 
+// Configurations (n-blocks per workgroup x waves x k-blocks per batch) are
+// from a sweep over the 8B shapes.  The K partition -- 16 waves per
+// workgroup and the K-split count -- depends only on the GEMM shape, never
+// on the number of row tiles, so every output element is summed in the same
+// order whether a window is verified alone or in a batch (bit-identical
+// results); only the n-blocks per workgroup shrink for more row tiles, to
+// bound register use.
+constexpr int kWaves = 16;
+
 template <int MT, int EPI>
 hipError_t launch_bf16(const GemmArgs& a, hipStream_t s) {
-  if (a.Nb <= 768) return launch_bf16_cfg<MT, EPI, 1, 16>(a, s);
-  if (a.Nb <= 4096) return launch_bf16_cfg<MT, EPI, 1, 8>(a, s);
-  return launch_bf16_cfg<MT, EPI, 2, 8>(a, s);
+  if constexpr (MT >= 2) return launch_bf16_cfg<MT, EPI, 2, kWaves, 2>(a, s);
+  else if constexpr (EPI == EPI_QKV) return launch_bf16_cfg<MT, EPI, 2, kWaves, 4>(a, s);
+  else return launch_bf16_cfg<MT, EPI, 4, kWaves, 2>(a, s);
 }
 
 template <int MT, int EPI>
 hipError_t launch_f32(const GemmArgs& a, hipStream_t s) {
   constexpr int NBW = 1, NW = 4;
-  const int grid = (a.Nb + NBW - 1) / NBW;
+  const int grid = ((a.Nb + NBW - 1) / NBW) * a.S;
   hipLaunchKernelGGL((k_gemm_f32<MT, NBW, NW, EPI>), dim3(grid), dim3(NW * 64), 0, s, a);
   return hipGetLastError();
 }
@@ -299,11 +315,21 @@ hipError_t launch_epi(int wtype, int mt, const GemmArgs& a, hipStream_t s) {
 
 }  // namespace
 
+int gemm_part_splits(int wtype, int Nb, int Kb, int mt) {
+  (void)mt;   // the split must not depend on the row count (batch invariance)
+  if (wtype != W_BF16) return 1;
+  const int groups = (Nb + 3) / 4;
+  int S = std::max(1, std::min(kMaxSplits, 256 / std::max(1, groups)));
+  while (S > 1 && Kb / S < kWaves) --S;           // keep >= 1 k-block per wave
+  return S;
+}
+
 hipError_t launch_gemm(int wtype, int mt, const GemmArgs& a, hipStream_t s) {
   if (a.Nb <= 0 || a.M <= 0) return hipSuccess;
+  if (a.S < 1 || (a.S > 1 && a.epi.kind != EPI_PART)) return hipErrorInvalidValue;
   switch (a.epi.kind) {
     case EPI_STORE: return launch_epi<EPI_STORE>(wtype, mt, a, s);
-    case EPI_RESID: return launch_epi<EPI_RESID>(wtype, mt, a, s);
+    case EPI_PART: return launch_epi<EPI_PART>(wtype, mt, a, s);
     case EPI_QKV: return launch_epi<EPI_QKV>(wtype, mt, a, s);
     case EPI_SILU: return launch_epi<EPI_SILU>(wtype, mt, a, s);
   }

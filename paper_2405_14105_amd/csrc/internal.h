@@ -45,7 +45,10 @@ constexpr int kMaxMt = 4;          // at most 64 rows per forward chunk
 constexpr int kMaxRows = kMaxMt * 16;
 
 // gemm epilogues
-enum Epi : int { EPI_STORE = 0, EPI_RESID = 1, EPI_QKV = 2, EPI_SILU = 3 };
+// EPI_PART stores split s of a K-split GEMM into its own partial buffer
+// (out + s * part_stride); the residual stream is updated by the next
+// RMSNorm, which folds x += sum_s partial_s in split order.
+enum Epi : int { EPI_STORE = 0, EPI_PART = 1, EPI_QKV = 2, EPI_SILU = 3 };
 
 struct PackRef {        // an activation pack (hi/lo bf16, or fp32 in hi)
   void* hi;
@@ -61,9 +64,10 @@ struct RowMap {         // token row m -> (window, row within window, position)
 
 struct EpiArgs {
   int kind;
-  // EPI_STORE: out [M][ld]; EPI_RESID: x [M][ld] += acc
+  // EPI_STORE: out [M][ld]; EPI_PART: out [S][part_stride] holding [M][ld]
   float* out;
   int ld;
+  size_t part_stride;
   int n_valid;          // logical N (features) -- outputs beyond are dropped
   // EPI_QKV
   float* q_out;         // [M][n_heads*hd]
@@ -83,8 +87,12 @@ struct GemmArgs {
   const void* Xhi;
   const void* Xlo;
   int Nb, Kb, M;
+  int S;                // K splits across workgroups (EPI_PART only; else 1)
   EpiArgs epi;
 };
+// K split the launcher uses for an EPI_PART GEMM of this shape
+int gemm_part_splits(int wtype, int Nb, int Kb, int mt);
+constexpr int kMaxSplits = 4;
 
 // launchers (gemm.hip)
 hipError_t launch_gemm(int wtype, int mt, const GemmArgs& a, hipStream_t s);
@@ -114,9 +122,12 @@ struct EmbedArgs {
 };
 hipError_t launch_embed_norm(const EmbedArgs& a, hipStream_t s);
 
-// RMSNorm of x rows into a pack; also optional diagnostic copy of x
-hipError_t launch_rmsnorm_pack(const float* x, int M, int d, const float* gain, float eps,
-                               int wtype, PackRef pack, float* copy_out, hipStream_t s);
+// Residual fold and RMSNorm of x rows into a pack: x += sum of the S partial
+// buffers delta + s * delta_stride (S may be 0), then pack rmsnorm(x) * gain;
+// also an optional diagnostic copy of the updated x.
+hipError_t launch_rmsnorm_pack(float* x, const float* delta, int S, size_t delta_stride, int M, int d,
+                               const float* gain, float eps, int wtype, PackRef pack, float* copy_out,
+                               hipStream_t s);
 
 // attention (attention.hip)
 struct AttnArgs {

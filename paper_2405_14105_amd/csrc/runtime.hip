@@ -97,6 +97,7 @@ struct dsi_model {
   std::vector<void*> allocs;
   // forward workspace for up to kMaxRows rows
   float* x = nullptr;
+  float* delta = nullptr;       // [kMaxSplits][kMaxRows][d] K-split partial outputs
   PackRef pk_d{}, pk_q{}, pk_ff{};
   float* qbuf = nullptr;
   float2* rope = nullptr;
@@ -237,10 +238,12 @@ dsi_status run_forward(dsi_model* m, dsi_kv* kv, int window0, int B, int R, cons
   DSI_TRY(ensure(m->attn_o, nparts * m->hd * sizeof(float)));
   DSI_TRY(ensure(m->attn_ml, nparts * sizeof(float2)));
 
+  int last_splits = 0;
   for (int l = 0; l < m->L; ++l) {
     const LayerW& lw = m->layers[l];
     GemmArgs g{};
     g.M = M;
+    g.S = 1;
     // fused QKV + RoPE + KV append
     g.W = lw.wqkv;
     g.Xhi = m->pk_d.hi;
@@ -285,7 +288,8 @@ dsi_status run_forward(dsi_model* m, dsi_kv* kv, int window0, int B, int R, cons
       HIP_TRY(launch_attention(m->kvb, m->hd, aa, s));
     }
 
-    // O projection + residual
+    // O projection into K-split partials; the next RMSNorm adds them to x
+    const size_t dstride = (size_t)kMaxRows * m->d;
     GemmArgs go{};
     go.M = M;
     go.W = lw.wo;
@@ -293,20 +297,23 @@ dsi_status run_forward(dsi_model* m, dsi_kv* kv, int window0, int B, int R, cons
     go.Xlo = m->pk_q.lo;
     go.Nb = m->Nb_o;
     go.Kb = m->Kb_q;
-    go.epi.kind = EPI_RESID;
-    go.epi.out = m->x;
+    go.S = gemm_part_splits(m->wtype, m->Nb_o, m->Kb_q, mt);
+    go.epi.kind = EPI_PART;
+    go.epi.out = m->delta;
     go.epi.ld = m->d;
+    go.epi.part_stride = dstride;
     go.epi.n_valid = m->d;
     {
       Prof p(m, DSI_K_OPROJ);
       HIP_TRY(launch_gemm(m->wtype, mt, go, s));
     }
 
-    HIP_TRY(launch_rmsnorm_pack(m->x, M, m->d, lw.ffn_norm, m->cfg.rms_eps, m->wtype, m->pk_d,
-                                nullptr, s));
+    HIP_TRY(launch_rmsnorm_pack(m->x, m->delta, go.S, dstride, M, m->d, lw.ffn_norm, m->cfg.rms_eps,
+                                m->wtype, m->pk_d, nullptr, s));
     // gate/up + SwiGLU into the down-projection pack
     GemmArgs gu{};
     gu.M = M;
+    gu.S = 1;
     gu.W = lw.wgu;
     gu.Xhi = m->pk_d.hi;
     gu.Xlo = m->pk_d.lo;
@@ -319,7 +326,7 @@ dsi_status run_forward(dsi_model* m, dsi_kv* kv, int window0, int B, int R, cons
       Prof p(m, DSI_K_GATEUP);
       HIP_TRY(launch_gemm(m->wtype, mt, gu, s));
     }
-    // down + residual
+    // down projection into K-split partials
     GemmArgs gd{};
     gd.M = M;
     gd.W = lw.wdown;
@@ -327,26 +334,35 @@ dsi_status run_forward(dsi_model* m, dsi_kv* kv, int window0, int B, int R, cons
     gd.Xlo = m->pk_ff.lo;
     gd.Nb = m->Nb_down;
     gd.Kb = m->Kb_ff;
-    gd.epi.kind = EPI_RESID;
-    gd.epi.out = m->x;
+    gd.S = gemm_part_splits(m->wtype, m->Nb_down, m->Kb_ff, mt);
+    gd.epi.kind = EPI_PART;
+    gd.epi.out = m->delta;
     gd.epi.ld = m->d;
+    gd.epi.part_stride = dstride;
     gd.epi.n_valid = m->d;
     {
       Prof p(m, DSI_K_DOWN);
       HIP_TRY(launch_gemm(m->wtype, mt, gd, s));
     }
+    last_splits = gd.S;
 
     if (l + 1 < m->L) {
-      HIP_TRY(launch_rmsnorm_pack(m->x, M, m->d, m->layers[l + 1].attn_norm, m->cfg.rms_eps,
-                                  m->wtype, m->pk_d, hidden ? hidden + (size_t)(l + 1) * Md : nullptr,
-                                  s));
+      HIP_TRY(launch_rmsnorm_pack(m->x, m->delta, gd.S, dstride, M, m->d, m->layers[l + 1].attn_norm,
+                                  m->cfg.rms_eps, m->wtype, m->pk_d,
+                                  hidden ? hidden + (size_t)(l + 1) * Md : nullptr, s));
     }
   }
-  if (hidden && !logits)
-    HIP_TRY(launch_copy_rows(m->x, hidden + (size_t)m->L * Md, Md, s));
-  if (!logits) return DSI_OK;
+  const size_t dstride = (size_t)kMaxRows * m->d;
+  if (!logits) {
+    // fold the last residual update only when the caller wants hidden states
+    if (hidden)
+      HIP_TRY(launch_rmsnorm_pack(m->x, m->delta, last_splits, dstride, M, m->d, m->final_norm,
+                                  m->cfg.rms_eps, m->wtype, m->pk_d, hidden + (size_t)m->L * Md, s));
+    return DSI_OK;
+  }
 
   GemmArgs gh{};
+  gh.S = 1;
   gh.W = m->lm_head;
   gh.Xhi = m->pk_d.hi;
   gh.Xlo = m->pk_d.lo;
@@ -358,12 +374,14 @@ dsi_status run_forward(dsi_model* m, dsi_kv* kv, int window0, int B, int R, cons
   gh.epi.n_valid = m->V;
   Prof ph(m, DSI_K_HEAD);
   if (head_last_only) {
-    HIP_TRY(launch_rmsnorm_pack(m->x + (size_t)(M - 1) * m->d, 1, m->d, m->final_norm,
+    const size_t off = (size_t)(M - 1) * m->d;
+    HIP_TRY(launch_rmsnorm_pack(m->x + off, m->delta + off, last_splits, dstride, 1, m->d, m->final_norm,
                                 m->cfg.rms_eps, m->wtype, m->pk_d, nullptr, s));
     gh.M = 1;
     HIP_TRY(launch_gemm(m->wtype, 1, gh, s));
   } else {
-    HIP_TRY(launch_rmsnorm_pack(m->x, M, m->d, m->final_norm, m->cfg.rms_eps, m->wtype, m->pk_d,
+    HIP_TRY(launch_rmsnorm_pack(m->x, m->delta, last_splits, dstride, M, m->d, m->final_norm,
+                                m->cfg.rms_eps, m->wtype, m->pk_d,
                                 hidden ? hidden + (size_t)m->L * Md : nullptr, s));
     gh.M = M;
     HIP_TRY(launch_gemm(m->wtype, mt, gh, s));
@@ -475,6 +493,7 @@ dsi_status dsi_model_create(const dsi_config* cfg, void* stream, dsi_model** out
     A(&w.wdown, (size_t)m->Nb_down * m->Kb_ff * tile * m->esz);
   }
   A((void**)&m->x, (size_t)kMaxRows * m->d * 4);
+  A((void**)&m->delta, (size_t)kMaxSplits * kMaxRows * m->d * 4);
   if (st == DSI_OK) m->pk_d = make_pack(m, m->Kb_d, &st);
   if (st == DSI_OK) m->pk_q = make_pack(m, m->Kb_q, &st);
   if (st == DSI_OK) m->pk_ff = make_pack(m, m->Kb_ff, &st);

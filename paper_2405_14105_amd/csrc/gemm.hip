@@ -269,20 +269,57 @@ hipError_t launch_bf16_cfg(GemmArgs a, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Configurations (n-blocks per workgroup x waves x k-blocks per batch) are
-// from a sweep over the 8B shapes.  The K partition -- 16 waves per
-// workgroup and the K-split count -- depends only on the GEMM shape, never
-// on the number of row tiles, so every output element is summed in the same
-// order whether a window is verified alone or in a batch (bit-identical
-// results); only the n-blocks per workgroup shrink for more row tiles, to
-// bound register use.
-constexpr int kWaves = 16;
+// Launch configurations per GEMM role (n-blocks per workgroup x waves x
+// k-blocks per batch), from a sweep over the 8B shapes.  The K partition --
+// the wave count and the K-split count -- depends only on the role and the
+// GEMM shape, never on the number of row tiles, so every output element is
+// summed in the same order whether a window is verified alone or in a batch
+// (bit-identical results).  Only the n-blocks per workgroup change with the
+// row-tile count (register budget) and with the output width: the gate/up
+// projection takes 7 n-blocks per workgroup when that makes exactly one
+// workgroup per CU (e.g. 1792 n-blocks on 256 CUs).
+template <int EPI>
+struct Role;
+template <>
+struct Role<EPI_QKV> {
+  static constexpr int NW = 16, U = 4;
+};
+template <>
+struct Role<EPI_PART> {
+  static constexpr int NW = 16, U = 2;
+};
+template <>
+struct Role<EPI_SILU> {
+  static constexpr int NW = 12, U = 1;
+};
+template <>
+struct Role<EPI_STORE> {
+  static constexpr int NW = 8, U = 2;
+};
+
+inline int part_nbw(int mt) { return mt >= 2 ? 2 : 4; }
+
+// CU rounds x n-blocks per workgroup: the time a CU spends streaming
+inline long cost_of(int Nb, int nbw) {
+  const long wgs = (Nb + nbw - 1) / nbw;
+  return ((wgs + 255) / 256) * nbw;
+}
 
 template <int MT, int EPI>
 hipError_t launch_bf16(const GemmArgs& a, hipStream_t s) {
-  if constexpr (MT >= 2) return launch_bf16_cfg<MT, EPI, 2, kWaves, 2>(a, s);
-  else if constexpr (EPI == EPI_QKV) return launch_bf16_cfg<MT, EPI, 2, kWaves, 4>(a, s);
-  else return launch_bf16_cfg<MT, EPI, 4, kWaves, 2>(a, s);
+  constexpr int NW = Role<EPI>::NW, U = Role<EPI>::U;
+  if constexpr (MT >= 2) {
+    return launch_bf16_cfg<MT, EPI, 2, NW, (U < 2 ? U : 2)>(a, s);
+  } else if constexpr (EPI == EPI_QKV) {
+    return launch_bf16_cfg<MT, EPI, 2, NW, U>(a, s);
+  } else if constexpr (EPI == EPI_PART) {
+    return launch_bf16_cfg<MT, EPI, 4, NW, U>(a, s);
+  } else if constexpr (EPI == EPI_SILU) {
+    if (cost_of(a.Nb, 7) < cost_of(a.Nb, 4)) return launch_bf16_cfg<MT, EPI, 7, NW, U>(a, s);
+    return launch_bf16_cfg<MT, EPI, 4, NW, U>(a, s);
+  } else {
+    return launch_bf16_cfg<MT, EPI, 6, NW, U>(a, s);
+  }
 }
 
 template <int MT, int EPI>
@@ -320,7 +357,7 @@ int gemm_part_splits(int wtype, int Nb, int Kb, int mt) {
   if (wtype != W_BF16) return 1;
   const int groups = (Nb + 3) / 4;
   int S = std::max(1, std::min(kMaxSplits, 256 / std::max(1, groups)));
-  while (S > 1 && Kb / S < kWaves) --S;           // keep >= 1 k-block per wave
+  while (S > 1 && Kb / S < Role<EPI_PART>::NW) --S;   // keep >= 1 k-block per wave
   return S;
 }
 

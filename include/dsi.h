@@ -208,6 +208,18 @@ enum {
 dsi_status dsi_profile_begin(dsi_model* m, int32_t kernel_class);
 dsi_status dsi_profile_end(dsi_model* m, int32_t* launches, double* total_ms);
 
+/* Time one GEMM kernel class (DSI_K_QKV, DSI_K_OPROJ, DSI_K_GATEUP,
+ * DSI_K_DOWN or DSI_K_HEAD) in isolation: `rounds` rounds, each launching
+ * that GEMM once per layer (once for the head) back to back on the model's
+ * stream with the row count and windows of the most recent dsi_verify,
+ * between one pair of HIP events.  Every launch streams its own layer's
+ * weights from HBM.  The launches read the library's current activation
+ * workspace and overwrite workspace outputs and dead KV rows beyond the
+ * committed lengths only.  Returns the number of launches and their average
+ * duration; synchronises the stream.  Diagnostics only. */
+dsi_status dsi_profile_kernel(dsi_model* m, dsi_kv* kv, int32_t kernel_class, int32_t rounds,
+                              int32_t* launches, double* avg_ms);
+
 /* Thread-local description of the last error. */
 const char* dsi_last_error(void);
 

@@ -110,6 +110,8 @@ struct dsi_model {
   int prof_class = 0;
   std::vector<hipEvent_t> prof_ev;
   size_t prof_used = 0;
+  // shape of the most recent verification forward (for dsi_profile_kernel)
+  int last_window0 = -1, last_B = 0, last_R = 0;
 };
 
 struct dsi_kv {
@@ -676,6 +678,9 @@ dsi_status dsi_verify(dsi_model* m, dsi_kv* kv, const dsi_verify_args* a, int32_
                   kv->hi[a->window0 + b], k + 1, kv->max_len);
   float* logits = a->d_logits_out ? a->d_logits_out : m->logits;
   DSI_TRY(run_forward(m, kv, a->window0, B, k + 1, a->d_tokens, logits, 0, a->d_hidden_out));
+  m->last_window0 = a->window0;
+  m->last_B = B;
+  m->last_R = k + 1;
   VerifyArgs va{};
   va.B = B;
   va.k = k;
@@ -786,6 +791,73 @@ dsi_status dsi_profile_end(dsi_model* m, int32_t* launches, double* total_ms) {
   *total_ms = tot;
   m->prof_class = 0;
   m->prof_used = 0;
+  return DSI_OK;
+}
+
+dsi_status dsi_profile_kernel(dsi_model* m, dsi_kv* kv, int32_t cls, int32_t rounds, int32_t* launches,
+                              double* avg_ms) {
+  if (!m || !kv || kv->m != m || !launches || !avg_ms || rounds < 1)
+    return fail(DSI_EINVAL, "bad argument");
+  if (m->last_B < 1 || m->last_window0 + m->last_B > kv->n_windows)
+    return fail(DSI_ESTATE, "run dsi_verify on this cache first");
+  if (cls != DSI_K_QKV && cls != DSI_K_OPROJ && cls != DSI_K_GATEUP && cls != DSI_K_DOWN && cls != DSI_K_HEAD)
+    return fail(DSI_EINVAL, "kernel class %d is not a GEMM class", cls);
+  const int M = m->last_B * m->last_R, mt = cdiv(M, 16);
+  const size_t dstride = (size_t)kMaxRows * m->d;
+  hipStream_t s = m->stream;
+  auto one = [&](int l) -> dsi_status {
+    GemmArgs g{};
+    g.M = M;
+    g.S = 1;
+    const LayerW& lw = m->layers[l < 0 ? 0 : l];
+    switch (cls) {
+      case DSI_K_QKV:
+        g.W = lw.wqkv; g.Xhi = m->pk_d.hi; g.Xlo = m->pk_d.lo; g.Nb = m->Nb_qkv; g.Kb = m->Kb_d;
+        g.epi.kind = EPI_QKV; g.epi.q_out = m->qbuf;
+        g.epi.kcache = kv_ptr(kv, kv->k, l, 0); g.epi.vcache = kv_ptr(kv, kv->v, l, 0);
+        g.epi.kv_bf16 = m->kvb; g.epi.n_heads = m->hq; g.epi.n_kv = m->hkv; g.epi.hd = m->hd;
+        g.epi.maxlen = kv->maxlen_pad; g.epi.rope = m->rope;
+        g.epi.rows = RowMap{kv->lens, m->last_window0, m->last_R};
+        break;
+      case DSI_K_OPROJ:
+      case DSI_K_DOWN:
+        g.W = cls == DSI_K_OPROJ ? lw.wo : lw.wdown;
+        g.Xhi = cls == DSI_K_OPROJ ? m->pk_q.hi : m->pk_ff.hi;
+        g.Xlo = cls == DSI_K_OPROJ ? m->pk_q.lo : m->pk_ff.lo;
+        g.Nb = cls == DSI_K_OPROJ ? m->Nb_o : m->Nb_down;
+        g.Kb = cls == DSI_K_OPROJ ? m->Kb_q : m->Kb_ff;
+        g.S = gemm_part_splits(m->wtype, g.Nb, g.Kb, mt);
+        g.epi.kind = EPI_PART; g.epi.out = m->delta; g.epi.ld = m->d; g.epi.part_stride = dstride;
+        g.epi.n_valid = m->d;
+        break;
+      case DSI_K_GATEUP:
+        g.W = lw.wgu; g.Xhi = m->pk_d.hi; g.Xlo = m->pk_d.lo; g.Nb = m->Nb_gu; g.Kb = m->Kb_d;
+        g.epi.kind = EPI_SILU; g.epi.pack = m->pk_ff; g.epi.ff = m->ff;
+        break;
+      default:
+        g.W = m->lm_head; g.Xhi = m->pk_d.hi; g.Xlo = m->pk_d.lo; g.Nb = m->Nb_head; g.Kb = m->Kb_d;
+        g.epi.kind = EPI_STORE; g.epi.out = m->logits; g.epi.ld = m->V; g.epi.n_valid = m->V;
+        break;
+    }
+    HIP_TRY(launch_gemm(m->wtype, mt, g, s));
+    return DSI_OK;
+  };
+  const int per_round = cls == DSI_K_HEAD ? 1 : m->L;
+  DSI_TRY(one(cls == DSI_K_HEAD ? -1 : 0));   // warm-up launch
+  hipEvent_t e0, e1;
+  HIP_TRY(hipEventCreate(&e0));
+  HIP_TRY(hipEventCreate(&e1));
+  HIP_TRY(hipEventRecord(e0, s));
+  for (int r = 0; r < rounds; ++r)
+    for (int l = 0; l < per_round; ++l) DSI_TRY(one(cls == DSI_K_HEAD ? -1 : l));
+  HIP_TRY(hipEventRecord(e1, s));
+  HIP_TRY(hipEventSynchronize(e1));
+  float ms = 0.f;
+  HIP_TRY(hipEventElapsedTime(&ms, e0, e1));
+  hipEventDestroy(e0);
+  hipEventDestroy(e1);
+  *launches = rounds * per_round;
+  *avg_ms = (double)ms / (rounds * per_round);
   return DSI_OK;
 }
 

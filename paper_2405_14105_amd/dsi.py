@@ -27,7 +27,7 @@ EXPORTED = (
     "dsi_model_create", "dsi_model_set_tensor", "dsi_model_destroy", "dsi_kv_create",
     "dsi_kv_destroy", "dsi_prefill", "dsi_verify", "dsi_accept", "dsi_kv_rollback",
     "dsi_kv_length", "dsi_sync", "dsi_kv_export", "dsi_kv_import", "dsi_kv_set_length",
-    "dsi_profile_begin", "dsi_profile_end", "dsi_last_error",
+    "dsi_profile_begin", "dsi_profile_end", "dsi_profile_kernel", "dsi_last_error",
 )
 DSI_K_QKV, DSI_K_ATTN, DSI_K_OPROJ, DSI_K_GATEUP, DSI_K_DOWN, DSI_K_HEAD, DSI_K_VERIFY = range(1, 8)
 
@@ -86,6 +86,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "dsi_kv_set_length": ([P, I32, I32], I32),
         "dsi_profile_begin": ([P, I32], I32),
         "dsi_profile_end": ([P, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_double)], I32),
+        "dsi_profile_kernel": ([P, P, I32, I32, ctypes.POINTER(ctypes.c_int32),
+                                ctypes.POINTER(ctypes.c_double)], I32),
         "dsi_last_error": ([], ctypes.c_char_p),
     }
     for name, (args, res) in sig.items():
@@ -193,6 +195,14 @@ def dsi_profile_end(model: int):
     n = ctypes.c_int32()
     t = ctypes.c_double()
     _check(load().dsi_profile_end(model, ctypes.byref(n), ctypes.byref(t)))
+    return n.value, t.value
+
+
+def dsi_profile_kernel(model: int, kv: int, kernel_class: int, rounds: int = 3):
+    """Returns (launches, avg_ms) of one GEMM class replayed back to back."""
+    n = ctypes.c_int32()
+    t = ctypes.c_double()
+    _check(load().dsi_profile_kernel(model, kv, kernel_class, rounds, ctypes.byref(n), ctypes.byref(t)))
     return n.value, t.value
 
 

@@ -19,7 +19,6 @@ import os
 import sys
 import threading
 import time
-from concurrent.futures import ThreadPoolExecutor
 
 import numpy as np
 
@@ -89,25 +88,17 @@ def measured_traffic(workload: str):
 # ------------------------------------------------------------------ GPU part
 def build_model(dsi, loader, shape, stream, n_windows, max_len):
     model = dsi.dsi_model_create(loader.config_for(shape), stream)
-    names = [(-1, n) for n in S.GLOBAL_TENSORS] + [(l, n) for l in range(shape.n_layers)
-                                                    for n in S.LAYER_TENSORS]
 
-    def make(item):
-        l, n = item
-        w = S.weight(shape, SEED, l, n)
-        return S.f32_to_bf16_bits(w) if shape.wdtype == "bf16" else w
+    def make(l, n):
+        return S.weight_bf16_bits(shape, SEED, l, n) if shape.wdtype == "bf16" else \
+            S.weight(shape, SEED, l, n)
+
+    def progress(l):
+        if (l + 1) % 8 == 0:
+            log(f"uploaded layer {l + 1}/{shape.n_layers} ({time.time() - t0:.1f}s)")
 
     t0 = time.time()
-    # generate the next tensor on a helper thread while the current uploads
-    with ThreadPoolExecutor(2) as ex:
-        fut = ex.submit(make, names[0])
-        for i, (l, n) in enumerate(names):
-            a = np.ascontiguousarray(fut.result())
-            if i + 1 < len(names):
-                fut = ex.submit(make, names[i + 1])
-            dsi.dsi_model_set_tensor(model, l, dsi.TENSOR_IDS[n], a.ctypes.data, a.nbytes, False)
-            if l >= 0 and n == "w_down" and (l + 1) % 8 == 0:
-                log(f"uploaded layer {l + 1}/{shape.n_layers} ({time.time() - t0:.1f}s)")
+    loader.upload(model, shape, make, progress)
     kv = dsi.dsi_kv_create(model, n_windows, max_len)
     return model, kv
 

@@ -138,7 +138,8 @@ _CHUNK_ELEMS = 1 << 22
 _POOL_THREADS = max(1, min(16, os.cpu_count() or 1))
 
 
-def _normal_rows(seed: int, layer: int, tid: int, shape: tuple, std: float) -> np.ndarray:
+def _normal_rows(seed: int, layer: int, tid: int, shape: tuple, std: float,
+                 bf16: bool = False) -> np.ndarray:
     rows = shape[0]
     cols = int(np.prod(shape[1:])) if len(shape) > 1 else 1
     out = np.empty((rows, cols), dtype=np.float32)
@@ -151,6 +152,11 @@ def _normal_rows(seed: int, layer: int, tid: int, shape: tuple, std: float) -> n
         g = _rng(seed, _S_WEIGHT, layer + 1, tid, ci)
         g.standard_normal(out=out[r0:r1], dtype=np.float32)
         out[r0:r1] *= np.float32(std)
+        if bf16:
+            # round-to-nearest-even to bf16, in place (same result as f32_to_bf16_bits)
+            u = out[r0:r1].view(np.uint32)
+            u += np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))
+            u &= np.uint32(0xFFFF0000)
 
     if len(starts) == 1:
         fill(0)
@@ -172,15 +178,30 @@ def weight(s: Shape, seed: int, layer: int, name: str) -> np.ndarray:
         else:
             g = (1.0 + 0.1 * _rng(seed, _S_GAIN, layer + 1, tid).standard_normal(shp)).astype(np.float32)
         return _bits_to_f32(f32_to_bf16_bits(g)) if s.wdtype == "bf16" else g
-    w = _normal_rows(seed, layer, tid, shp, 0.02)
-    if s.wdtype == "bf16":
-        w = _bits_to_f32(f32_to_bf16_bits(w))
-    return w
+    return _normal_rows(seed, layer, tid, shp, 0.02, bf16=(s.wdtype == "bf16"))
 
 
 def weight_bf16_bits(s: Shape, seed: int, layer: int, name: str) -> np.ndarray:
     """bf16 bit patterns (uint16) of weight(); exact, since the values are bf16."""
-    return f32_to_bf16_bits(weight(s, seed, layer, name))
+    w = weight(s, seed, layer, name)
+    if s.wdtype != "bf16":
+        return f32_to_bf16_bits(w)
+    # the low halves are zero: keep the high 16 bits of each (little-endian) fp32
+    flat = w.reshape(-1).view(np.uint16)
+    out = np.empty(w.size, dtype=np.uint16)
+    step = _CHUNK_ELEMS
+    spans = [(i, min(w.size, i + step)) for i in range(0, w.size, step)]
+
+    def cut(span):
+        a, b = span
+        out[a:b] = flat[2 * a + 1:2 * b:2]
+
+    if len(spans) == 1:
+        cut(spans[0])
+    else:
+        with ThreadPoolExecutor(min(_POOL_THREADS, len(spans))) as ex:
+            list(ex.map(cut, spans))
+    return out.reshape(w.shape)
 
 
 def all_weights(s: Shape, seed: int) -> dict:

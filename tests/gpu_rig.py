@@ -12,19 +12,20 @@ from paper_2405_14105_amd import dsi, loader
 
 def host_tensor_fn(shape, seed):
     def fn(layer, name):
-        w = S.weight(shape, seed, layer, name)
-        return S.f32_to_bf16_bits(w) if shape.wdtype == "bf16" else w
+        if shape.wdtype == "bf16":
+            return S.weight_bf16_bits(shape, seed, layer, name)
+        return S.weight(shape, seed, layer, name)
     return fn
 
 
 class Rig:
-    def __init__(self, shape, seed: int, n_windows: int, max_len: int):
+    def __init__(self, shape, seed: int, n_windows: int, max_len: int, progress=None):
         self.shape = shape
         self.seed = seed
         self.dev = torch.device("cuda:0")
         self.stream = torch.cuda.current_stream().cuda_stream
         self.model = dsi.dsi_model_create(loader.config_for(shape), self.stream)
-        loader.upload(self.model, shape, host_tensor_fn(shape, seed))
+        loader.upload(self.model, shape, host_tensor_fn(shape, seed), progress)
         self.kv = dsi.dsi_kv_create(self.model, n_windows, max_len)
         self._keep = []
 

@@ -15,58 +15,15 @@ import pytest
 import torch
 
 import dsi_synth as S
-from oracle import forward64, verify64
+from oracle import forward64
 from paper_2405_14105_amd import dsi
 
 from gpu_rig import Rig
+from parity import TOL, e2e_check, getter, oracle_logits, split_check
 
 pytestmark = pytest.mark.gpu
 
 SEED = 0
-TOL = {"f32": 1e-4, "bf16": 2e-2}
-
-
-def getter(shape, seed=SEED):
-    cache = {}
-
-    def get(layer, name):
-        if (layer, name) not in cache:
-            cache[(layer, name)] = S.weight(shape, seed, layer, name).astype(np.float64)
-        return cache[(layer, name)]
-    return get
-
-
-def oracle_logits(shape, prefix, window_tokens, return_hidden=False):
-    toks = np.concatenate([np.asarray(prefix, np.int64), np.asarray(window_tokens, np.int64)])
-    res = forward64(shape, getter(shape), toks, return_hidden=return_hidden)
-    L = len(prefix)
-    if return_hidden:
-        return res[0][L:], res[2][:, L:]
-    return res[0][L:]
-
-
-def split_check(z, tokens, q, u, n, tok, mode="sample"):
-    r = verify64(z, tokens[1:], q, u, mode=mode)
-    if r.accept_margin < 1e-4 or r.draw_margin < 1e-9:
-        return None
-    assert (int(n), int(tok)) == (r.n, r.token)
-    return r
-
-
-def e2e_check(zo, delta, tokens, q, u, n, tok, mode="sample"):
-    r = verify64(zo, tokens[1:], q, u, mode=mode)
-    if mode == "sample":
-        lnflag = 2.0 * delta + 1e-6
-        if any(abs(np.log(max(r.a[i], 1e-300)) - np.log(max(float(u[i]), 1e-300))) < lnflag
-               for i in range(min(r.n + 1, len(r.a)))):
-            return None
-        if r.accept_margin < 1e-4 or r.draw_margin < 4.0 * delta + 1e-9:
-            return None
-    else:
-        if r.accept_margin <= 2.0 * delta:
-            return None
-    assert (int(n), int(tok)) == (r.n, r.token)
-    return r
 
 
 CASES = [

@@ -1,0 +1,244 @@
+"""Parity at the full workload sizes, in the launch configuration the
+benchmark times (same seeded weights, prefixes and window inputs).
+
+The fp64 oracle cannot run a 32-layer model over a 2059-token sequence in
+seconds, so at the 8B and 13B shapes it checks outputs it can compute one by
+one, teacher-forced on the GPU's own state:
+  * layer l (sampled layers): the oracle applies layer l to the residual rows
+    the GPU fed into it (hidden dump) against the GPU's cached prefix K/V
+    (kv export), and must reproduce the GPU's K/V rows for the window and
+    the residual rows leaving the layer;
+  * LM head: the oracle's final RMSNorm + head on the GPU's last residual rows
+    against every GPU logit;
+  * verification: the oracle's accept/reject on the GPU's full-vocabulary
+    logits (split check), sampling, greedy and the bonus path (q = p);
+  * KV state: commit length, rollback and bit-identical re-verification,
+    batch invariance of the 7-window batch.
+The 1B shape is checked end to end: the oracle's full forward over the prefix
+and window against the GPU's logits.
+"""
+import time
+
+import numpy as np
+import pytest
+import torch
+
+import dsi_synth as S
+from oracle import head64, layer64, softmax64
+from paper_2405_14105_amd import dsi
+
+from gpu_rig import Rig
+from parity import TOL, e2e_check, getter, oracle_logits, split_check
+
+pytestmark = [pytest.mark.gpu, pytest.mark.fullsize, pytest.mark.timeout(900)]
+
+SEED = 0
+# Teacher-forced per-layer gate: GPU activations are fp32-accurate (hi/lo bf16
+# operands, fp32 accumulation), i.e. ~1e-5 relative per layer; 1e-3 of the
+# rows' magnitude leaves a 100x margin and still fails on any wrong term.
+LAYER_REL_TOL = 1e-3
+HEAD_TOL = 1e-3
+
+
+def say(msg):
+    print(msg, flush=True)
+
+
+def ulps_bf16(g, o):
+    """|g - o| in units of the bf16 spacing at o (both bf16 values)."""
+    e = np.frexp(np.abs(o))[1]
+    return np.abs(g - o) / np.ldexp(1.0, e - 8)
+
+
+def check_layer(rig, shape, window, layer, L, hidden, rows):
+    """Teacher-forced check of one layer for one window's rows."""
+    R = len(rows)
+    kg, vg = rig.export_kv(window, layer, L + R)
+    x_in = hidden[layer][rows].astype(np.float64)
+    x_gpu = hidden[layer + 1][rows].astype(np.float64)
+    pos = np.arange(L, L + R)
+    get = getter(shape, SEED, cache=False)
+    x_o, k_o, v_o = layer64(shape, get, layer, x_in, pos, kg[:L], vg[:L])
+    err = float(np.abs(x_gpu - x_o).max())
+    scale = max(1.0, float(np.abs(x_o).max()))
+    stats = []
+    for nm, g, o in (("K", kg[L:], k_o), ("V", vg[L:], v_o)):
+        d = np.abs(g - o)
+        # error of the unrounded values, relative to the head row's magnitude
+        rowmax = np.abs(o).max(axis=-1, keepdims=True)
+        rel = d / np.maximum(rowmax, 1e-30)
+        i = np.unravel_index(int(np.argmax(rel)), rel.shape)
+        stats.append((nm, float(np.mean(d > 0)), float(ulps_bf16(g, o).max()), float(rel.max()),
+                      i, float(g[i]), float(o[i]), float(rowmax[i[:2]][0])))
+    say(f"  layer {layer} window {window}: max|dx| = {err:.3g} (scale {scale:.3g}); " +
+        "; ".join(f"{nm}: flips {fr:.4f}, max {mu:.1f} ulp, max rel {rl:.2e} at {ix} "
+                  f"gpu {gv:.6g} oracle {ov:.6g} rowmax {rm:.3g}"
+                  for nm, fr, mu, rl, ix, gv, ov, rm in stats))
+    for nm, fr, mu, rl, *_ in stats:
+        # bf16 rows: equal up to rounding flips, i.e. one bf16 spacing of the
+        # row's largest entry (2^-7 relative) at most, and rarely
+        assert rl <= 2.0 ** -7 and fr < 0.01, (nm, layer, rl, fr)
+    assert err <= LAYER_REL_TOL * scale, (layer, err, scale)
+    return err
+
+
+def check_head(shape, hidden_last, logits, rows):
+    zo = head64(shape, getter(shape, SEED, cache=False), hidden_last[rows].astype(np.float64))
+    err = float(np.abs(logits[rows] - zo).max())
+    say(f"  head: max|dz| = {err:.3g} over {len(rows)} rows x {shape.vocab}")
+    assert err <= HEAD_TOL
+    return err
+
+
+def check_verify(logits, tokens, q, u, n, tok, k, mode="sample"):
+    r = split_check(logits, tokens, q, u, n, tok, mode=mode)
+    assert 0 <= int(n) <= k and 0 <= int(tok) < logits.shape[1]
+    return r
+
+
+# ----------------------------------------------------------------- 1B, L 512, k 5
+def test_1b_L512_k5_end_to_end():
+    shape = S.SHAPES["llama1b"]
+    L, k = 512, 5
+    t0 = time.time()
+    with Rig(shape, SEED, 1, L + 2 * (k + 1)) as rig:
+        prefix = S.prefix_tokens(shape, SEED, 0, L)
+        rig.prefill(0, prefix)
+        wi = S.window_inputs(shape, SEED, 1, k)
+        toks, q, u = wi["tokens"], wi["q"], wi["u"]
+        out = rig.verify(0, toks, q, u, commit=True)
+        assert rig.length(0) == L + out["n"][0] + 1
+        dsi.dsi_kv_rollback(rig.kv, 0, L)
+        g = rig.verify(0, toks, mode=dsi.DSI_GREEDY, commit=False)
+        assert np.array_equal(g["logits"], out["logits"])
+    say(f"  GPU done ({time.time() - t0:.1f}s)")
+    zo = oracle_logits(shape, prefix, toks[0], seed=SEED, cache=False)
+    delta = float(np.abs(out["logits"] - zo).max())
+    say(f"  1B end to end: max|dz| = {delta:.3g} ({time.time() - t0:.1f}s)")
+    assert delta <= TOL["bf16"]
+    check_verify(out["logits"], toks[0], q[0], u[0], out["n"][0], out["token"][0], k)
+    e2e_check(zo, delta, toks[0], q[0], u[0], out["n"][0], out["token"][0])
+    check_verify(g["logits"], toks[0], None, None, g["n"][0], g["token"][0], k, mode="greedy")
+    e2e_check(zo, delta, toks[0], None, None, g["n"][0], g["token"][0], mode="greedy")
+
+
+# ------------------------------------------------- 8B: one window L 2048 k 10, and 7 windows
+L8, K8 = 2048, 10
+LENS7, K7 = [1024 + i for i in range(7)], 5
+
+
+@pytest.fixture(scope="module")
+def rig8b():
+    shape = S.SHAPES["llama8b"]
+    t0 = time.time()
+    rig = Rig(shape, SEED, 8, L8 + 2 * (K8 + 1),
+              progress=lambda l: (l + 1) % 8 == 0 and say(f"  8B upload layer {l + 1} "
+                                                          f"({time.time() - t0:.0f}s)"))
+    prefixes = {0: S.prefix_tokens(shape, SEED, 0, L8)}
+    for i, Lb in enumerate(LENS7):
+        prefixes[1 + i] = S.prefix_tokens(shape, SEED, 1 + i, Lb)
+    for w, p in prefixes.items():
+        rig.prefill(w, p)
+    say(f"  8B model ready ({time.time() - t0:.1f}s)")
+    yield rig
+    rig.close()
+
+
+def test_8b_L2048_k10_layers_head_and_verify(rig8b):
+    rig, shape = rig8b, rig8b.shape
+    wi = S.window_inputs(shape, SEED, 1, K8)
+    toks, q, u = wi["tokens"], wi["q"], wi["u"]
+    out = rig.verify(0, toks, q, u, commit=False, want_hidden=True)
+    hid, z = out["hidden"], out["logits"]
+    rows = np.arange(K8 + 1)
+    for layer in (0, shape.n_layers // 2, shape.n_layers - 1):
+        check_layer(rig, shape, 0, layer, L8, hid, rows)
+    check_head(shape, hid[shape.n_layers], z, rows)
+    check_verify(z, toks[0], q[0], u[0], out["n"][0], out["token"][0], K8)
+    g = rig.verify(0, toks, mode=dsi.DSI_GREEDY, commit=False)
+    assert np.array_equal(g["logits"], z)
+    check_verify(z, toks[0], None, None, g["n"][0], g["token"][0], K8, mode="greedy")
+    assert rig.length(0) == L8
+
+
+def test_8b_L2048_k10_bonus_commit_rollback(rig8b):
+    rig, shape = rig8b, rig8b.shape
+    wi = S.window_inputs(shape, SEED, 1, K8)
+    toks, u = wi["tokens"], wi["u"]
+    base = rig.verify(0, toks, wi["q"], u, commit=False)
+    z = base["logits"]
+    # drafter = target (q = p): every draft is accepted up to rounding of q
+    # to fp32, so the bonus path is taken at full vocabulary
+    q = np.stack([softmax64(z[i]) for i in range(K8)]).astype(np.float32)[None]
+    out = rig.verify(0, toks, q, u, commit=True)
+    r = check_verify(z, toks[0], q[0], u[0], out["n"][0], out["token"][0], K8)
+    if r is not None:
+        assert r.n == K8
+    n = int(out["n"][0])
+    assert rig.length(0) == L8 + n + 1
+    # rows of w0 and the accepted drafts stay; rollback restores the prefix
+    dsi.dsi_kv_rollback(rig.kv, 0, L8)
+    assert rig.length(0) == L8
+    again = rig.verify(0, toks, wi["q"], u, commit=False)
+    assert np.array_equal(again["logits"], z)
+    assert (again["n"][0], again["token"][0]) == (base["n"][0], base["token"][0])
+
+
+def test_8b_x7_L1024_k5_batched(rig8b):
+    rig, shape = rig8b, rig8b.shape
+    B, k, V = len(LENS7), K7, shape.vocab
+    wi = S.window_inputs(shape, SEED, B, k, window0=1)
+    toks, q, u = wi["tokens"], wi["q"], wi["u"]
+    out = rig.verify(1, toks, q, u, commit=False, want_hidden=True)
+    zz = out["logits"].reshape(B, k + 1, V)
+    for b in range(B):
+        check_verify(zz[b], toks[b], q[b], u[b], out["n"][b], out["token"][b], k)
+    # teacher-forced first and last layer for the shortest and longest window
+    for b in (0, B - 1):
+        rows = np.arange(b * (k + 1), (b + 1) * (k + 1))
+        for layer in (0, shape.n_layers - 1):
+            check_layer(rig, shape, 1 + b, layer, LENS7[b], out["hidden"], rows)
+        check_head(shape, out["hidden"][shape.n_layers], out["logits"], rows)
+    # batch invariance: each window alone gives bit-identical logits and decisions
+    for b in range(B):
+        one = rig.verify(1 + b, toks[b:b + 1], q[b:b + 1], u[b:b + 1], commit=False)
+        assert np.array_equal(one["logits"], zz[b]), b
+        assert (one["n"][0], one["token"][0]) == (out["n"][b], out["token"][b])
+    # committing the batch advances every window by its own n + 1
+    res = rig.verify(1, toks, q, u, commit=True)
+    for b in range(B):
+        assert rig.length(1 + b) == LENS7[b] + res["n"][b] + 1
+        dsi.dsi_kv_rollback(rig.kv, 1 + b, LENS7[b])
+        assert rig.length(1 + b) == LENS7[b]
+
+
+# ------------------------------------------------------------ 13B MHA, L 32768, k 10
+def test_13b_L32768_k10_long_prefix_and_rollback():
+    shape = S.SHAPES["llama13b"]
+    L, k = 32768, 10
+    t0 = time.time()
+    with Rig(shape, SEED, 1, L + 2 * (k + 1),
+             progress=lambda l: (l + 1) % 10 == 0 and say(f"  13B upload layer {l + 1} "
+                                                          f"({time.time() - t0:.0f}s)")) as rig:
+        rig.prefill(0, S.prefix_tokens(shape, SEED, 0, L))
+        say(f"  13B prefill done ({time.time() - t0:.1f}s)")
+        wi = S.window_inputs(shape, SEED, 1, k)
+        toks, q, u = wi["tokens"], wi["q"], wi["u"]
+        out = rig.verify(0, toks, q, u, commit=True, want_hidden=True)
+        n = int(out["n"][0])
+        assert rig.length(0) == L + n + 1
+        check_verify(out["logits"], toks[0], q[0], u[0], n, out["token"][0], k)
+        rows = np.arange(k + 1)
+        for layer in (0, shape.n_layers - 1):
+            check_layer(rig, shape, 0, layer, L, out["hidden"], rows)
+        check_head(shape, out["hidden"][shape.n_layers], out["logits"], rows)
+        # a second window on top of the accepted tokens, then roll both back
+        wi2 = S.window_inputs(shape, SEED + 1, 1, k)
+        o2 = rig.verify(0, wi2["tokens"], wi2["q"], wi2["u"], commit=True)
+        assert rig.length(0) == L + n + 1 + int(o2["n"][0]) + 1
+        dsi.dsi_kv_rollback(rig.kv, 0, L)
+        assert rig.length(0) == L
+        again = rig.verify(0, toks, q, u, commit=False)
+        assert np.array_equal(again["logits"], out["logits"])
+        assert (again["n"][0], again["token"][0]) == (out["n"][0], out["token"][0])
+    say(f"  13B done ({time.time() - t0:.1f}s)")

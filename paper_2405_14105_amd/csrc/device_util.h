@@ -69,6 +69,23 @@ __device__ __forceinline__ void pack_store(const PackRef& p, int wtype, int m, i
   }
 }
 
+// store 4 consecutive features f0..f0+3 (f0 % 4 == 0) of token m: 8 bytes
+// per half for bf16 packs, 16 bytes for fp32 packs
+__device__ __forceinline__ void pack_store4(const PackRef& p, int wtype, int m, int f0, const float* v) {
+  const size_t idx = pack_index(p.Kb, m, f0);
+  if (wtype == W_BF16) {
+    uint16_t hi[4], lo[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) split_bf16(v[e], hi[e], lo[e]);
+    *(uint2*)((uint16_t*)p.hi + idx) = uint2{(uint32_t)hi[0] | ((uint32_t)hi[1] << 16),
+                                             (uint32_t)hi[2] | ((uint32_t)hi[3] << 16)};
+    *(uint2*)((uint16_t*)p.lo + idx) = uint2{(uint32_t)lo[0] | ((uint32_t)lo[1] << 16),
+                                             (uint32_t)lo[2] | ((uint32_t)lo[3] << 16)};
+  } else {
+    *(float4*)((float*)p.hi + idx) = float4{v[0], v[1], v[2], v[3]};
+  }
+}
+
 // store 8 consecutive features f0..f0+7 (f0 % 8 == 0) of token m: one
 // 16-byte store per half for bf16 packs, two for fp32 packs
 __device__ __forceinline__ void pack_store8(const PackRef& p, int wtype, int m, int f0, const float* v) {

@@ -138,8 +138,11 @@ __global__ __launch_bounds__(256) void k_embed_norm(EmbedArgs a) {
   }
 }
 
+// S (compile time) partials are folded in split order; every load of a row
+// group is issued before the sums so they are in flight together.
+template <int S>
 __global__ __launch_bounds__(256) void k_rmsnorm_pack(float* __restrict__ x, const float* __restrict__ delta,
-                                                       int S, size_t dstride, int d,
+                                                       size_t dstride, int d,
                                                        const float* __restrict__ gain, float eps,
                                                        int wtype, PackRef pack, float* copy_out) {
   __shared__ float sh[4];
@@ -152,13 +155,14 @@ __global__ __launch_bounds__(256) void k_rmsnorm_pack(float* __restrict__ x, con
     if (g < ng) {
       const size_t off = (size_t)m * d + 8 * g;
       load8(x, W_F32, off, v[i]);
-      if (S > 0) {
-        for (int sp = 0; sp < S; ++sp) {
-          float p[8];
-          load8(delta + sp * dstride, W_F32, off, p);
+      if constexpr (S > 0) {
+        float p[S][8];
 #pragma unroll
-          for (int e = 0; e < 8; ++e) v[i][e] += p[e];
-        }
+        for (int sp = 0; sp < S; ++sp) load8(delta + sp * dstride, W_F32, off, p[sp]);
+#pragma unroll
+        for (int sp = 0; sp < S; ++sp)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[i][e] += p[sp][e];
         float* xr = x + off;
         *(float4*)xr = float4{v[i][0], v[i][1], v[i][2], v[i][3]};
         *(float4*)(xr + 4) = float4{v[i][4], v[i][5], v[i][6], v[i][7]};
@@ -261,8 +265,18 @@ hipError_t launch_embed_norm(const EmbedArgs& a, hipStream_t s) {
 hipError_t launch_rmsnorm_pack(float* x, const float* delta, int S, size_t delta_stride, int M, int d,
                                const float* gain, float eps, int wtype, PackRef pack, float* copy_out,
                                hipStream_t s) {
-  hipLaunchKernelGGL(k_rmsnorm_pack, dim3(M), dim3(256), 0, s, x, delta, S, delta_stride, d, gain, eps,
-                     wtype, pack, copy_out);
+#define DSI_NORM_LAUNCH(SS)                                                                       \
+  hipLaunchKernelGGL(k_rmsnorm_pack<SS>, dim3(M), dim3(256), 0, s, x, delta, delta_stride, d, gain, eps, \
+                     wtype, pack, copy_out)
+  switch (S) {
+    case 0: DSI_NORM_LAUNCH(0); break;
+    case 1: DSI_NORM_LAUNCH(1); break;
+    case 2: DSI_NORM_LAUNCH(2); break;
+    case 3: DSI_NORM_LAUNCH(3); break;
+    case 4: DSI_NORM_LAUNCH(4); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef DSI_NORM_LAUNCH
   return hipGetLastError();
 }
 

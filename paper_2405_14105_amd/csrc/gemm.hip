@@ -22,8 +22,32 @@ namespace dsi {
 
 namespace {
 
+// EPI_RESID inputs of the one epilogue item a thread owns (residual and gain
+// values), loaded before the main loop so that their latency is hidden.
+struct ResidIn {
+  float4 x, g;
+};
+template <int MT, int NBW, int NW>
+__device__ __forceinline__ ResidIn resid_prefetch(const GemmArgs& a, int nb0) {
+  static_assert(NBW * MT <= NW, "finish() must give each thread at most one item");
+  ResidIn r{};
+  const int it = threadIdx.x;
+  if (it < NBW * MT * 64) {
+    const int l = it & 63, jm = it >> 6;
+    const int nb = nb0 + jm / MT, m = (jm % MT) * 16 + (l & 15);
+    if (nb < a.Nb && m < a.M) {
+      const int n0 = nb * 16 + (l >> 4) * 4;
+      r.x = *(const float4*)(a.epi.x + (size_t)m * a.epi.ld + n0);
+      r.g = *(const float4*)(a.epi.gain + n0);
+    }
+  }
+  return r;
+}
+
+// Returns the sum of the squared residual values it wrote (EPI_RESID), else 0.
 template <int WT, int EPI>
-__device__ __forceinline__ void epilogue(const EpiArgs& e, int nb, int r0, int m, int split, f32x4 s) {
+__device__ __forceinline__ float epilogue(const EpiArgs& e, int nb, int r0, int m, int split, f32x4 s,
+                                          const ResidIn& pre) {
   switch (EPI) {
     case EPI_STORE: {
 #pragma unroll
@@ -100,13 +124,43 @@ __device__ __forceinline__ void epilogue(const EpiArgs& e, int nb, int r0, int m
       }
       break;
     }
+    case EPI_RESID: {
+      // four consecutive features n0..n0+3 of row m (x, gain prefetched)
+      const int n0 = nb * 16 + r0;
+      const float xn[4] = {pre.x.x + s[0], pre.x.y + s[1], pre.x.z + s[2], pre.x.w + s[3]};
+      *(float4*)(e.x + (size_t)m * e.ld + n0) = float4{xn[0], xn[1], xn[2], xn[3]};
+      const float y[4] = {xn[0] * pre.g.x, xn[1] * pre.g.y, xn[2] * pre.g.z, xn[3] * pre.g.w};
+      pack_store4(e.pack, WT, m, n0, y);
+      return xn[0] * xn[0] + xn[1] * xn[1] + xn[2] * xn[2] + xn[3] * xn[3];
+    }
+  }
+  return 0.f;
+}
+
+// RMSNorm scale of each input row from the per-n-block sums of squares the
+// producing GEMM wrote (EPI_RESID, layout [row][ssq_n]):
+// rs[m] = 1/sqrt(sum_nb ssq[m][nb] / d + eps).  One wave per row: lane l sums
+// entries l, l+64, ... and a butterfly finishes, a fixed order that does not
+// depend on the number of rows.
+template <int NW>
+__device__ __forceinline__ void row_scales(const GemmArgs& a, float* rs) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  for (int m = w; m < a.M; m += NW) {
+    const float* p = a.ssq + (size_t)m * a.ssq_n;
+    float sum = 0.f;
+#pragma unroll 4
+    for (int i = lane; i < a.ssq_n; i += 64) sum += p[i];
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) sum += __shfl_xor(sum, off);
+    if (lane == 0) rs[m] = 1.0f / sqrtf(sum / (float)a.norm_d + a.eps);
   }
 }
 
-// Sum the NW per-wave partial tiles in wave order (deterministic) and run the
-// epilogue on this workgroup's n-blocks.
+// rs: per-row RMSNorm scales (row_scales) or nullptr.  The iteration count
+// is uniform across a wave, so the EPI_RESID lane reduction is safe.
 template <int WT, int EPI, int MT, int NBW, int NW>
-__device__ __forceinline__ void finish(const GemmArgs& a, const f32x4* red, int nb0, int split) {
+__device__ __forceinline__ void finish(const GemmArgs& a, const f32x4* red, const float* rs, int nb0,
+                                       int split, const ResidIn& pre) {
   constexpr int ACC = NBW * MT;
   for (int it = threadIdx.x; it < ACC * 64; it += NW * 64) {
     const int l = it & 63, jm = it >> 6;
@@ -114,7 +168,16 @@ __device__ __forceinline__ void finish(const GemmArgs& a, const f32x4* red, int 
     f32x4 v = red[jm * 64 + l];
     for (int ww = 1; ww < NW; ++ww) v += red[(ww * ACC + jm) * 64 + l];
     const int nb = nb0 + j, m = t * 16 + (l & 15);
-    if (nb < a.Nb && m < a.M) epilogue<WT, EPI>(a.epi, nb, (l >> 4) * 4, m, split, v);
+    const bool ok = nb < a.Nb && m < a.M;
+    if (ok && rs) v *= rs[m];
+    float sq = 0.f;
+    if (ok) sq = epilogue<WT, EPI>(a.epi, nb, (l >> 4) * 4, m, split, v, pre);
+    if constexpr (EPI == EPI_RESID) {
+      // lanes l, l+16, l+32, l+48 hold the 16 features of row m
+      sq += __shfl_xor(sq, 16);
+      sq += __shfl_xor(sq, 32);
+      if (ok && l < 16) a.epi.ssq[(size_t)m * a.Nb + nb] = sq;
+    }
   }
 }
 
@@ -142,6 +205,7 @@ template <int MT, int NBW, int NW, int U, int EPI>
 __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(GemmArgs a) {
   constexpr int ACC = NBW * MT;
   __shared__ f32x4 red[NW * ACC * 64];
+  __shared__ float rs[kMaxRows];
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
   const Work wk = work_of<NBW, NW>(a);
@@ -169,6 +233,9 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(GemmArgs a) {
       }
   };
   if (kb_beg < kb_end) load_w(cur, kb_beg);
+  ResidIn pre{};
+  if constexpr (EPI == EPI_RESID) pre = resid_prefetch<MT, NBW, NW>(a, nb0);
+  if (a.ssq) row_scales<NW>(a, rs);   // overlaps the first weight loads
   for (int kb = kb_beg; kb < kb_end; kb += U) {
     u32x4 nxt[U][NBW];
     if (kb + U < kb_end) load_w(nxt, kb + U);
@@ -202,19 +269,23 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(GemmArgs a) {
 #pragma unroll
     for (int t = 0; t < MT; ++t) red[((w * NBW + j) * MT + t) * 64 + lane] = acc[j][t];
   __syncthreads();
-  finish<W_BF16, EPI, MT, NBW, NW>(a, red, nb0, wk.split);
+  finish<W_BF16, EPI, MT, NBW, NW>(a, red, a.ssq ? rs : nullptr, nb0, wk.split, pre);
 }
 
 template <int MT, int NBW, int NW, int EPI>
 __global__ __launch_bounds__(NW * 64) void k_gemm_f32(GemmArgs a) {
   constexpr int ACC = NBW * MT;
   __shared__ f32x4 red[NW * ACC * 64];
+  __shared__ float rs[kMaxRows];
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
   const Work wk = work_of<NBW, NW>(a);
   const int nb0 = wk.nb0, nbv = wk.nbv, kb_beg = wk.kb_beg, kb_end = wk.kb_end;
   const float4* __restrict__ W = (const float4*)a.W;
   const float4* __restrict__ X = (const float4*)a.Xhi;
+  ResidIn pre{};
+  if constexpr (EPI == EPI_RESID) pre = resid_prefetch<MT, NBW, NW>(a, nb0);
+  if (a.ssq) row_scales<NW>(a, rs);
 
   f32x4 acc[NBW][MT];
 #pragma unroll
@@ -252,7 +323,7 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_f32(GemmArgs a) {
 #pragma unroll
     for (int t = 0; t < MT; ++t) red[((w * NBW + j) * MT + t) * 64 + lane] = acc[j][t];
   __syncthreads();
-  finish<W_F32, EPI, MT, NBW, NW>(a, red, nb0, wk.split);
+  finish<W_F32, EPI, MT, NBW, NW>(a, red, a.ssq ? rs : nullptr, nb0, wk.split, pre);
 }
 
 // Grid shaping.  Each wave reuses every activation fragment it loads across
@@ -296,6 +367,10 @@ template <>
 struct Role<EPI_STORE> {
   static constexpr int NW = 8, U = 2;
 };
+template <>
+struct Role<EPI_RESID> {
+  static constexpr int NW = 16, U = 4;
+};
 
 inline int part_nbw(int mt) { return mt >= 2 ? 2 : 4; }
 
@@ -314,6 +389,8 @@ hipError_t launch_bf16(const GemmArgs& a, hipStream_t s) {
     return launch_bf16_cfg<MT, EPI, 2, NW, U>(a, s);
   } else if constexpr (EPI == EPI_PART) {
     return launch_bf16_cfg<MT, EPI, 4, NW, U>(a, s);
+  } else if constexpr (EPI == EPI_RESID) {
+    return launch_bf16_cfg<MT, EPI, 1, NW, U>(a, s);
   } else if constexpr (EPI == EPI_SILU) {
     if (cost_of(a.Nb, 7) < cost_of(a.Nb, 4)) return launch_bf16_cfg<MT, EPI, 7, NW, U>(a, s);
     return launch_bf16_cfg<MT, EPI, 4, NW, U>(a, s);
@@ -369,6 +446,7 @@ hipError_t launch_gemm(int wtype, int mt, const GemmArgs& a, hipStream_t s) {
     case EPI_PART: return launch_epi<EPI_PART>(wtype, mt, a, s);
     case EPI_QKV: return launch_epi<EPI_QKV>(wtype, mt, a, s);
     case EPI_SILU: return launch_epi<EPI_SILU>(wtype, mt, a, s);
+    case EPI_RESID: return launch_epi<EPI_RESID>(wtype, mt, a, s);
   }
   return hipErrorInvalidValue;
 }

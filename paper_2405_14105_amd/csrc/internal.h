@@ -48,7 +48,13 @@ constexpr int kMaxRows = kMaxMt * 16;
 // EPI_PART stores split s of a K-split GEMM into its own partial buffer
 // (out + s * part_stride); the residual stream is updated by the next
 // RMSNorm, which folds x += sum_s partial_s in split order.
-enum Epi : int { EPI_STORE = 0, EPI_PART = 1, EPI_QKV = 2, EPI_SILU = 3 };
+// EPI_RESID (no K split) adds the product to the residual stream in place,
+// x[m][n] += y, writes the next RMSNorm's input before scaling, x * gain,
+// into the consumer's activation pack, and stores the sum of x^2 over the
+// 16 features of each n-block in ssq[m * Nb + nb].  The consuming
+// GEMM (GemmArgs::ssq) forms the RMSNorm scale of each row from those sums
+// and applies it to its accumulators: W (x * g) / rms(x) = W RMSNorm(x).
+enum Epi : int { EPI_STORE = 0, EPI_PART = 1, EPI_QKV = 2, EPI_SILU = 3, EPI_RESID = 4 };
 
 struct PackRef {        // an activation pack (hi/lo bf16, or fp32 in hi)
   void* hi;
@@ -77,9 +83,12 @@ struct EpiArgs {
   int n_heads, n_kv, hd, maxlen;
   const float2* rope;   // [M][hd/2] (cos, sin)
   RowMap rows;
-  // EPI_SILU
+  // EPI_SILU (pack, ff), EPI_RESID (pack, x, gain, ssq; out unused)
   PackRef pack;
   int ff;
+  float* x;             // [M][ld] residual stream, updated in place
+  const float* gain;    // [ld] gain of the RMSNorm that consumes x
+  float* ssq;           // [M][Nb] per-n-block sums of x^2
 };
 
 struct GemmArgs {
@@ -89,6 +98,11 @@ struct GemmArgs {
   int Nb, Kb, M;
   int S;                // K splits across workgroups (EPI_PART only; else 1)
   EpiArgs epi;
+  // optional RMSNorm of the input rows (the pack holds x * gain): the
+  // accumulators of row m are scaled by 1/sqrt(sum_nb ssq[m][nb] / norm_d + eps)
+  const float* ssq;     // [M][ssq_n] or nullptr
+  int ssq_n, norm_d;
+  float eps;
 };
 // K split the launcher uses for an EPI_PART GEMM of this shape
 int gemm_part_splits(int wtype, int Nb, int Kb, int mt);

@@ -98,6 +98,7 @@ struct dsi_model {
   // forward workspace for up to kMaxRows rows
   float* x = nullptr;
   float* delta = nullptr;       // [kMaxSplits][kMaxRows][d] K-split partial outputs
+  float* ssq = nullptr;         // [kMaxRows][Nb_o] per-n-block sums of x^2 (EPI_RESID)
   PackRef pk_d{}, pk_q{}, pk_ff{};
   float* qbuf = nullptr;
   float2* rope = nullptr;
@@ -191,6 +192,109 @@ struct Prof {
 
 // ------------------------------------------------------------- forward plan
 //
+// GEMM arguments of each kernel class of layer l over M rows, shared by the
+// forward and the profiling replay.
+//   QKV     attn-normed pack pk_d -> q, K/V cache (RoPE, append)
+//   O       attention pack pk_q -> x += o W_o^T (in place), pk_d = x * g_ffn,
+//           per-n-block sums of x^2 (EPI_RESID)
+//   gate/up pk_d scaled by the RMSNorm of x (ssq) -> SwiGLU pack pk_ff
+//   down    pk_ff -> K-split partials, folded into x by the next RMSNorm
+//   head    final-normed pack pk_d -> logits
+GemmArgs qkv_args(dsi_model* m, dsi_kv* kv, int l, int M, RowMap rows) {
+  GemmArgs g{};
+  g.M = M;
+  g.S = 1;
+  g.W = m->layers[l].wqkv;
+  g.Xhi = m->pk_d.hi;
+  g.Xlo = m->pk_d.lo;
+  g.Nb = m->Nb_qkv;
+  g.Kb = m->Kb_d;
+  g.epi.kind = EPI_QKV;
+  g.epi.q_out = m->qbuf;
+  g.epi.kcache = kv_ptr(kv, kv->k, l, 0);
+  g.epi.vcache = kv_ptr(kv, kv->v, l, 0);
+  g.epi.kv_bf16 = m->kvb;
+  g.epi.n_heads = m->hq;
+  g.epi.n_kv = m->hkv;
+  g.epi.hd = m->hd;
+  g.epi.maxlen = kv->maxlen_pad;
+  g.epi.rope = m->rope;
+  g.epi.rows = rows;
+  return g;
+}
+
+GemmArgs oproj_args(dsi_model* m, int l, int M) {
+  GemmArgs g{};
+  g.M = M;
+  g.S = 1;
+  g.W = m->layers[l].wo;
+  g.Xhi = m->pk_q.hi;
+  g.Xlo = m->pk_q.lo;
+  g.Nb = m->Nb_o;
+  g.Kb = m->Kb_q;
+  g.epi.kind = EPI_RESID;
+  g.epi.x = m->x;
+  g.epi.ld = m->d;
+  g.epi.n_valid = m->d;
+  g.epi.gain = m->layers[l].ffn_norm;
+  g.epi.pack = m->pk_d;
+  g.epi.ssq = m->ssq;
+  return g;
+}
+
+GemmArgs gateup_args(dsi_model* m, int l, int M) {
+  GemmArgs g{};
+  g.M = M;
+  g.S = 1;
+  g.W = m->layers[l].wgu;
+  g.Xhi = m->pk_d.hi;
+  g.Xlo = m->pk_d.lo;
+  g.Nb = m->Nb_gu;
+  g.Kb = m->Kb_d;
+  g.epi.kind = EPI_SILU;
+  g.epi.pack = m->pk_ff;
+  g.epi.ff = m->ff;
+  g.ssq = m->ssq;
+  g.ssq_n = m->Nb_o;
+  g.norm_d = m->d;
+  g.eps = m->cfg.rms_eps;
+  return g;
+}
+
+GemmArgs down_args(dsi_model* m, int l, int M, int mt) {
+  GemmArgs g{};
+  g.M = M;
+  g.W = m->layers[l].wdown;
+  g.Xhi = m->pk_ff.hi;
+  g.Xlo = m->pk_ff.lo;
+  g.Nb = m->Nb_down;
+  g.Kb = m->Kb_ff;
+  g.S = gemm_part_splits(m->wtype, m->Nb_down, m->Kb_ff, mt);
+  g.epi.kind = EPI_PART;
+  g.epi.out = m->delta;
+  g.epi.ld = m->d;
+  g.epi.part_stride = (size_t)kMaxRows * m->d;
+  g.epi.n_valid = m->d;
+  return g;
+}
+
+GemmArgs head_args(dsi_model* m, float* logits, int M) {
+  GemmArgs g{};
+  g.M = M;
+  g.S = 1;
+  g.W = m->lm_head;
+  g.Xhi = m->pk_d.hi;
+  g.Xlo = m->pk_d.lo;
+  g.Nb = m->Nb_head;
+  g.Kb = m->Kb_d;
+  g.epi.kind = EPI_STORE;
+  g.epi.out = logits;
+  g.epi.ld = m->V;
+  g.epi.n_valid = m->V;
+  return g;
+}
+
+//
 // One target forward over M = B * R rows: R consecutive rows of each of the
 // B windows window0..window0+B-1, appended after each window's cached
 // length.  Writes the rows' K/V into the cache (the window length itself is
@@ -241,31 +345,12 @@ dsi_status run_forward(dsi_model* m, dsi_kv* kv, int window0, int B, int R, cons
   DSI_TRY(ensure(m->attn_ml, nparts * sizeof(float2)));
 
   int last_splits = 0;
+  const size_t dstride = (size_t)kMaxRows * m->d;
   for (int l = 0; l < m->L; ++l) {
-    const LayerW& lw = m->layers[l];
-    GemmArgs g{};
-    g.M = M;
-    g.S = 1;
     // fused QKV + RoPE + KV append
-    g.W = lw.wqkv;
-    g.Xhi = m->pk_d.hi;
-    g.Xlo = m->pk_d.lo;
-    g.Nb = m->Nb_qkv;
-    g.Kb = m->Kb_d;
-    g.epi.kind = EPI_QKV;
-    g.epi.q_out = m->qbuf;
-    g.epi.kcache = kv_ptr(kv, kv->k, l, 0);
-    g.epi.vcache = kv_ptr(kv, kv->v, l, 0);
-    g.epi.kv_bf16 = m->kvb;
-    g.epi.n_heads = m->hq;
-    g.epi.n_kv = m->hkv;
-    g.epi.hd = m->hd;
-    g.epi.maxlen = kv->maxlen_pad;
-    g.epi.rope = m->rope;
-    g.epi.rows = rows;
     {
       Prof p(m, DSI_K_QKV);
-      HIP_TRY(launch_gemm(m->wtype, mt, g, s));
+      HIP_TRY(launch_gemm(m->wtype, mt, qkv_args(m, kv, l, M, rows), s));
     }
 
     AttnArgs aa{};
@@ -290,58 +375,18 @@ dsi_status run_forward(dsi_model* m, dsi_kv* kv, int window0, int B, int R, cons
       HIP_TRY(launch_attention(m->kvb, m->hd, aa, s));
     }
 
-    // O projection into K-split partials; the next RMSNorm adds them to x
-    const size_t dstride = (size_t)kMaxRows * m->d;
-    GemmArgs go{};
-    go.M = M;
-    go.W = lw.wo;
-    go.Xhi = m->pk_q.hi;
-    go.Xlo = m->pk_q.lo;
-    go.Nb = m->Nb_o;
-    go.Kb = m->Kb_q;
-    go.S = gemm_part_splits(m->wtype, m->Nb_o, m->Kb_q, mt);
-    go.epi.kind = EPI_PART;
-    go.epi.out = m->delta;
-    go.epi.ld = m->d;
-    go.epi.part_stride = dstride;
-    go.epi.n_valid = m->d;
+    // O projection: residual update in place, FFN-norm input for gate/up
     {
       Prof p(m, DSI_K_OPROJ);
-      HIP_TRY(launch_gemm(m->wtype, mt, go, s));
+      HIP_TRY(launch_gemm(m->wtype, mt, oproj_args(m, l, M), s));
     }
-
-    HIP_TRY(launch_rmsnorm_pack(m->x, m->delta, go.S, dstride, M, m->d, lw.ffn_norm, m->cfg.rms_eps,
-                                m->wtype, m->pk_d, nullptr, s));
-    // gate/up + SwiGLU into the down-projection pack
-    GemmArgs gu{};
-    gu.M = M;
-    gu.S = 1;
-    gu.W = lw.wgu;
-    gu.Xhi = m->pk_d.hi;
-    gu.Xlo = m->pk_d.lo;
-    gu.Nb = m->Nb_gu;
-    gu.Kb = m->Kb_d;
-    gu.epi.kind = EPI_SILU;
-    gu.epi.pack = m->pk_ff;
-    gu.epi.ff = m->ff;
+    // gate/up (RMSNorm scale applied to the accumulators) + SwiGLU
     {
       Prof p(m, DSI_K_GATEUP);
-      HIP_TRY(launch_gemm(m->wtype, mt, gu, s));
+      HIP_TRY(launch_gemm(m->wtype, mt, gateup_args(m, l, M), s));
     }
     // down projection into K-split partials
-    GemmArgs gd{};
-    gd.M = M;
-    gd.W = lw.wdown;
-    gd.Xhi = m->pk_ff.hi;
-    gd.Xlo = m->pk_ff.lo;
-    gd.Nb = m->Nb_down;
-    gd.Kb = m->Kb_ff;
-    gd.S = gemm_part_splits(m->wtype, m->Nb_down, m->Kb_ff, mt);
-    gd.epi.kind = EPI_PART;
-    gd.epi.out = m->delta;
-    gd.epi.ld = m->d;
-    gd.epi.part_stride = dstride;
-    gd.epi.n_valid = m->d;
+    const GemmArgs gd = down_args(m, l, M, mt);
     {
       Prof p(m, DSI_K_DOWN);
       HIP_TRY(launch_gemm(m->wtype, mt, gd, s));
@@ -354,7 +399,6 @@ dsi_status run_forward(dsi_model* m, dsi_kv* kv, int window0, int B, int R, cons
                                   hidden ? hidden + (size_t)(l + 1) * Md : nullptr, s));
     }
   }
-  const size_t dstride = (size_t)kMaxRows * m->d;
   if (!logits) {
     // fold the last residual update only when the caller wants hidden states
     if (hidden)
@@ -363,17 +407,7 @@ dsi_status run_forward(dsi_model* m, dsi_kv* kv, int window0, int B, int R, cons
     return DSI_OK;
   }
 
-  GemmArgs gh{};
-  gh.S = 1;
-  gh.W = m->lm_head;
-  gh.Xhi = m->pk_d.hi;
-  gh.Xlo = m->pk_d.lo;
-  gh.Nb = m->Nb_head;
-  gh.Kb = m->Kb_d;
-  gh.epi.kind = EPI_STORE;
-  gh.epi.out = logits;
-  gh.epi.ld = m->V;
-  gh.epi.n_valid = m->V;
+  GemmArgs gh = head_args(m, logits, M);
   Prof ph(m, DSI_K_HEAD);
   if (head_last_only) {
     const size_t off = (size_t)(M - 1) * m->d;
@@ -496,6 +530,7 @@ dsi_status dsi_model_create(const dsi_config* cfg, void* stream, dsi_model** out
   }
   A((void**)&m->x, (size_t)kMaxRows * m->d * 4);
   A((void**)&m->delta, (size_t)kMaxSplits * kMaxRows * m->d * 4);
+  A((void**)&m->ssq, (size_t)m->Nb_o * kMaxRows * 4);
   if (st == DSI_OK) m->pk_d = make_pack(m, m->Kb_d, &st);
   if (st == DSI_OK) m->pk_q = make_pack(m, m->Kb_q, &st);
   if (st == DSI_OK) m->pk_ff = make_pack(m, m->Kb_ff, &st);
@@ -805,39 +840,15 @@ dsi_status dsi_profile_kernel(dsi_model* m, dsi_kv* kv, int32_t cls, int32_t rou
   const int M = m->last_B * m->last_R, mt = cdiv(M, 16);
   const size_t dstride = (size_t)kMaxRows * m->d;
   hipStream_t s = m->stream;
+  const RowMap rows{kv->lens, m->last_window0, m->last_R};
   auto one = [&](int l) -> dsi_status {
-    GemmArgs g{};
-    g.M = M;
-    g.S = 1;
-    const LayerW& lw = m->layers[l < 0 ? 0 : l];
+    GemmArgs g;
     switch (cls) {
-      case DSI_K_QKV:
-        g.W = lw.wqkv; g.Xhi = m->pk_d.hi; g.Xlo = m->pk_d.lo; g.Nb = m->Nb_qkv; g.Kb = m->Kb_d;
-        g.epi.kind = EPI_QKV; g.epi.q_out = m->qbuf;
-        g.epi.kcache = kv_ptr(kv, kv->k, l, 0); g.epi.vcache = kv_ptr(kv, kv->v, l, 0);
-        g.epi.kv_bf16 = m->kvb; g.epi.n_heads = m->hq; g.epi.n_kv = m->hkv; g.epi.hd = m->hd;
-        g.epi.maxlen = kv->maxlen_pad; g.epi.rope = m->rope;
-        g.epi.rows = RowMap{kv->lens, m->last_window0, m->last_R};
-        break;
-      case DSI_K_OPROJ:
-      case DSI_K_DOWN:
-        g.W = cls == DSI_K_OPROJ ? lw.wo : lw.wdown;
-        g.Xhi = cls == DSI_K_OPROJ ? m->pk_q.hi : m->pk_ff.hi;
-        g.Xlo = cls == DSI_K_OPROJ ? m->pk_q.lo : m->pk_ff.lo;
-        g.Nb = cls == DSI_K_OPROJ ? m->Nb_o : m->Nb_down;
-        g.Kb = cls == DSI_K_OPROJ ? m->Kb_q : m->Kb_ff;
-        g.S = gemm_part_splits(m->wtype, g.Nb, g.Kb, mt);
-        g.epi.kind = EPI_PART; g.epi.out = m->delta; g.epi.ld = m->d; g.epi.part_stride = dstride;
-        g.epi.n_valid = m->d;
-        break;
-      case DSI_K_GATEUP:
-        g.W = lw.wgu; g.Xhi = m->pk_d.hi; g.Xlo = m->pk_d.lo; g.Nb = m->Nb_gu; g.Kb = m->Kb_d;
-        g.epi.kind = EPI_SILU; g.epi.pack = m->pk_ff; g.epi.ff = m->ff;
-        break;
-      default:
-        g.W = m->lm_head; g.Xhi = m->pk_d.hi; g.Xlo = m->pk_d.lo; g.Nb = m->Nb_head; g.Kb = m->Kb_d;
-        g.epi.kind = EPI_STORE; g.epi.out = m->logits; g.epi.ld = m->V; g.epi.n_valid = m->V;
-        break;
+      case DSI_K_QKV: g = qkv_args(m, kv, l, M, rows); break;
+      case DSI_K_OPROJ: g = oproj_args(m, l, M); break;
+      case DSI_K_GATEUP: g = gateup_args(m, l, M); break;
+      case DSI_K_DOWN: g = down_args(m, l, M, mt); break;
+      default: g = head_args(m, m->logits, M); break;
     }
     HIP_TRY(launch_gemm(m->wtype, mt, g, s));
     return DSI_OK;

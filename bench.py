@@ -74,6 +74,21 @@ def gateup_bytes(shape, M) -> int:
     return 2 * shape.d_ff * shape.d_model * esz + M * shape.d_model * 4 + M * shape.d_ff * 4
 
 
+def gemm_bytes(shape, M) -> dict:
+    """Algorithmic bytes of one launch of each GEMM class: the weight matrix,
+    the input rows (fp32-equivalent) and the output rows."""
+    s = shape
+    esz = 2 if s.wdtype == "bf16" else 4
+    d, qkv = s.d_model, s.q_dim + 2 * s.kv_dim
+
+    def b(n_out, n_in, out_bytes):
+        return n_out * n_in * esz + M * n_in * 4 + M * out_bytes
+
+    return {"qkv": b(qkv, d, qkv * 4), "o_proj": b(d, s.q_dim, 2 * d * 4),
+            "gate_up": gateup_bytes(s, M), "down": b(d, s.d_ff, d * 4),
+            "head": b(s.vocab, d, s.vocab * 4)}
+
+
 def measured_traffic(workload: str):
     import hashlib
     h = hashlib.sha256()
@@ -113,6 +128,9 @@ def run_gpu(args, wl):
     dev = torch.device("cuda:0")
     shape, k, lens = wl.shape, wl.k, list(wl.prefix_lens)
     B = len(lens)
+    # a stream of its own (default priority): the library captures the
+    # verification step into a graph on non-null streams
+    torch.cuda.set_stream(torch.cuda.Stream())
     stream = torch.cuda.current_stream().cuda_stream
     if args.copy_calibration:
         a = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
@@ -182,12 +200,13 @@ def run_gpu(args, wl):
         kt[name] = {"launches_per_step": nl / args.steps, "avg_ms": tot / max(nl, 1),
                     "ms_per_step": tot / args.steps}
     log("per-class ms/step: " + ", ".join(f"{n} {v['ms_per_step']:.3f}" for n, v in kt.items()))
-    # the roofline kernel alone: every layer's gate/up GEMM back to back
+    # each GEMM class alone: every layer's launch replayed back to back
     step()
-    nl, avg = dsi.dsi_profile_kernel(model, kv, dsi.DSI_K_GATEUP, 5)
-    kt["gate_up"]["isolated_avg_ms"] = avg
-    kt["gate_up"]["isolated_launches"] = nl
-    log(f"gate/up GEMM alone: {nl} launches, {avg * 1e3:.2f} us each")
+    for name in ("qkv", "o_proj", "gate_up", "down", "head"):
+        nl, avg = dsi.dsi_profile_kernel(model, kv, classes[name], 5)
+        kt[name]["isolated_avg_ms"] = avg
+        kt[name]["isolated_launches"] = nl
+        log(f"{name} GEMM alone: {nl} launches, {avg * 1e3:.2f} us each")
     dsi.dsi_kv_destroy(kv)
     dsi.dsi_model_destroy(model)
     return {"ms": ms, "per_step": per, "kernels": kt, "n_accepted": n_acc.tolist()}
@@ -287,7 +306,8 @@ def main():
         print(json.dumps({"metric": METRIC, "ms_per_step": round(ms, 4), "note": "counter run"}))
         return
     gu = g["kernels"]["gate_up"]
-    gu_bytes = gateup_bytes(wl.shape, M)
+    gb = gemm_bytes(wl.shape, M)
+    gu_bytes = gb["gate_up"]
     achieved = gu_bytes / (gu["isolated_avg_ms"] * 1e-3) / 1e9
     roof = {"bound": "hbm", "kernel": "gate/up projection + SwiGLU (k_gemm_bf16 EPI_SILU)",
             "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -322,6 +342,9 @@ def main():
                      "achieved_GBs": round(sb["total"] / (ms * 1e-3) / 1e9, 1),
                      "frac_of_peak": round(sb["total"] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
         "kernels_ms_per_step": {n: round(v["ms_per_step"], 4) for n, v in g["kernels"].items()},
+        "gemm_isolated": {n: {"us": round(v["isolated_avg_ms"] * 1e3, 2),
+                              "GBs": round(gb[n] / (v["isolated_avg_ms"] * 1e-3) / 1e9, 1)}
+                          for n, v in g["kernels"].items() if "isolated_avg_ms" in v},
         "roofline": roof,
     }
     if not args.no_cpu_baseline:

@@ -26,8 +26,9 @@
  *    q(d) not positive and finite) make the affected window output
  *    n = -1, token = -1, leave its KV length unchanged, and make the next
  *    synchronising call (dsi_sync, dsi_kv_length) return DSI_EINVAL.
- *  - A dsi_model is immutable after its tensors are set and may be shared by
- *    several dsi_kv; a dsi_kv and its model's stream are single-threaded.
+ *  - A dsi_model's weights are immutable after they are set and the model
+ *    may serve several dsi_kv; calls on one model (and its KV caches) must
+ *    not overlap: the model's forward workspaces are shared by all of them.
  */
 #ifndef DSI_H
 #define DSI_H
@@ -93,7 +94,12 @@ enum {
 #define DSI_MAX_ROWS 64
 
 /* Create a model with device storage for every weight (zero until set).
- * stream: hipStream_t used by every call on this model and its KV caches. */
+ * stream: hipStream_t used by every call on this model and its KV caches.
+ * With a non-null stream, dsi_verify records its launches into a HIP graph
+ * the first time it sees a combination of arguments (pointers, sizes, mode,
+ * cache) and replays that graph on later calls with the same combination
+ * (up to 16 are cached per model; the environment variable DSI_GRAPHS=0
+ * read here disables this).  Results are identical either way. */
 dsi_status dsi_model_create(const dsi_config* cfg, void* stream, dsi_model** out);
 
 /* Upload one tensor (host memory if src_on_device == 0, else device memory).

@@ -348,7 +348,9 @@ hipError_t launch_bf16_cfg(GemmArgs a, hipStream_t s) {
 // (bit-identical results).  Only the n-blocks per workgroup change with the
 // row-tile count (register budget) and with the output width: the gate/up
 // projection takes 7 n-blocks per workgroup when that makes exactly one
-// workgroup per CU (e.g. 1792 n-blocks on 256 CUs).
+// workgroup per CU (e.g. 1792 n-blocks on 256 CUs); the LM head takes 12
+// (wide output, one k-block per batch).  Measured with 32 layers' weights
+// rotated so that no launch finds its weights in a cache.
 template <int EPI>
 struct Role;
 template <>
@@ -365,7 +367,7 @@ struct Role<EPI_SILU> {
 };
 template <>
 struct Role<EPI_STORE> {
-  static constexpr int NW = 8, U = 2;
+  static constexpr int NW = 8, U = 1;
 };
 template <>
 struct Role<EPI_RESID> {
@@ -395,7 +397,7 @@ hipError_t launch_bf16(const GemmArgs& a, hipStream_t s) {
     if (cost_of(a.Nb, 7) < cost_of(a.Nb, 4)) return launch_bf16_cfg<MT, EPI, 7, NW, U>(a, s);
     return launch_bf16_cfg<MT, EPI, 4, NW, U>(a, s);
   } else {
-    return launch_bf16_cfg<MT, EPI, 6, NW, U>(a, s);
+    return launch_bf16_cfg<MT, EPI, 12, NW, U>(a, s);
   }
 }
 

@@ -4,6 +4,7 @@
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <algorithm>
@@ -113,6 +114,15 @@ struct dsi_model {
   size_t prof_used = 0;
   // shape of the most recent verification forward (for dsi_profile_kernel)
   int last_window0 = -1, last_B = 0, last_R = 0;
+  // captured verification steps, keyed by every value their launches use
+  bool use_graphs = true;
+  struct Graph {
+    std::vector<uint64_t> key;
+    hipGraphExec_t exec = nullptr;
+    uint64_t used = 0;
+  };
+  std::vector<Graph> graphs;
+  uint64_t graph_clock = 0;
 };
 
 struct dsi_kv {
@@ -300,8 +310,34 @@ GemmArgs head_args(dsi_model* m, float* logits, int M) {
 // length.  Writes the rows' K/V into the cache (the window length itself is
 // advanced by the caller).  logits: nullptr (no head), else [M][V]
 // (head_last_only: only the last row, into logits[0..V)).
-dsi_status run_forward(dsi_model* m, dsi_kv* kv, int window0, int B, int R, const int* d_tokens,
-                       float* logits, int head_last_only, float* hidden) {
+// Attention partition of a forward: query tiles and key chunks.  Sized from
+// the host bound on lengths; allocates the chunk-partial buffers (so no
+// allocation happens while launches are being captured).
+struct AttnPlan {
+  int n_qtiles = 0, chunk = 0, n_chunks = 0;
+};
+
+dsi_status plan_attention(dsi_model* m, dsi_kv* kv, int window0, int B, int R, AttnPlan* p) {
+  long long kmax = 0;
+  for (int b = 0; b < B; ++b) kmax = std::max(kmax, kv->hi[window0 + b] + R);
+  // The chunk size depends only on the model, R and the cache capacity --
+  // never on B or the current lengths -- so a window's partial sums and
+  // therefore its results are identical alone or inside a batch.
+  const int G = m->hq / m->hkv;
+  p->n_qtiles = cdiv(G * R, 16);
+  const int want = std::max(1, cdiv(512, m->hkv * p->n_qtiles));
+  int chunk = (int)round_up((size_t)cdiv(kv->max_len, want), kAttnChunkQuantum);
+  p->chunk = std::min(std::max(chunk, kAttnChunkQuantum), 16384);
+  p->n_chunks = (int)((kmax + p->chunk - 1) / p->chunk);
+  const size_t nparts = (size_t)B * m->hkv * p->n_qtiles * p->n_chunks * 16;
+  DSI_TRY(ensure(m->attn_o, nparts * m->hd * sizeof(float)));
+  DSI_TRY(ensure(m->attn_ml, nparts * sizeof(float2)));
+  return DSI_OK;
+}
+
+// Stream-ordered launches only (capturable into a graph).
+dsi_status run_forward(dsi_model* m, dsi_kv* kv, const AttnPlan& ap, int window0, int B, int R,
+                       const int* d_tokens, float* logits, int head_last_only, float* hidden) {
   hipStream_t s = m->stream;
   const int M = B * R;
   const int mt = cdiv(M, 16);
@@ -327,23 +363,6 @@ dsi_status run_forward(dsi_model* m, dsi_kv* kv, int window0, int B, int R, cons
   ea.hidden0 = hidden;
   HIP_TRY(launch_embed_norm(ea, s));
 
-  // attention split over key chunks, sized from the host bound on lengths
-  long long kmax = 0;
-  for (int b = 0; b < B; ++b) kmax = std::max(kmax, kv->hi[window0 + b] + R);
-  // The chunk size depends only on the model, R and the cache capacity --
-  // never on B or the current lengths -- so a window's partial sums and
-  // therefore its results are identical alone or inside a batch.
-  const int G = m->hq / m->hkv;
-  const int n_qtiles = cdiv(G * R, 16);
-  const int zq = B * m->hkv * n_qtiles;
-  const int want = std::max(1, cdiv(512, m->hkv * n_qtiles));
-  int chunk = (int)round_up((size_t)cdiv(kv->max_len, want), kAttnChunkQuantum);
-  chunk = std::min(std::max(chunk, kAttnChunkQuantum), 16384);
-  const int n_chunks = (int)((kmax + chunk - 1) / chunk);
-  const size_t nparts = (size_t)zq * n_chunks * 16;
-  DSI_TRY(ensure(m->attn_o, nparts * m->hd * sizeof(float)));
-  DSI_TRY(ensure(m->attn_ml, nparts * sizeof(float2)));
-
   int last_splits = 0;
   const size_t dstride = (size_t)kMaxRows * m->d;
   for (int l = 0; l < m->L; ++l) {
@@ -362,9 +381,9 @@ dsi_status run_forward(dsi_model* m, dsi_kv* kv, int window0, int B, int R, cons
     aa.n_heads = m->hq;
     aa.n_kv = m->hkv;
     aa.maxlen = kv->maxlen_pad;
-    aa.n_qtiles = n_qtiles;
-    aa.chunk = chunk;
-    aa.n_chunks = n_chunks;
+    aa.n_qtiles = ap.n_qtiles;
+    aa.chunk = ap.chunk;
+    aa.n_chunks = ap.n_chunks;
     aa.scale = (float)(1.0 / sqrt((double)m->hd));
     aa.part_o = (float*)m->attn_o.p;
     aa.part_ml = (float2*)m->attn_ml.p;
@@ -465,6 +484,47 @@ dsi_status verify_args_ok(int B, int k, int V, const int* tokens, const float* q
   return DSI_OK;
 }
 
+// Launch a verification step through a cached graph: captured from the
+// stream on first use of a key, replayed afterwards (one submission instead
+// of a few hundred kernel launches).  At most kMaxGraphs are kept (least
+// recently used evicted).
+constexpr size_t kMaxGraphs = 16;
+
+template <typename F>
+dsi_status replay_or_capture(dsi_model* m, const std::vector<uint64_t>& key, F&& launches) {
+  ++m->graph_clock;
+  for (auto& g : m->graphs)
+    if (g.key == key) {
+      g.used = m->graph_clock;
+      HIP_TRY(hipGraphLaunch(g.exec, m->stream));
+      return DSI_OK;
+    }
+  HIP_TRY(hipStreamBeginCapture(m->stream, hipStreamCaptureModeThreadLocal));
+  const dsi_status st = launches();
+  hipGraph_t graph = nullptr;
+  const hipError_t e = hipStreamEndCapture(m->stream, &graph);
+  if (st != DSI_OK) {
+    if (graph) hipGraphDestroy(graph);
+    return st;
+  }
+  if (e != hipSuccess) return fail(DSI_EHIP, "graph capture: %s", hipGetErrorString(e));
+  hipGraphExec_t exec = nullptr;
+  const hipError_t ei = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+  hipGraphDestroy(graph);
+  if (ei != hipSuccess) return fail(DSI_EHIP, "graph instantiate: %s", hipGetErrorString(ei));
+  if (m->graphs.size() >= kMaxGraphs) {
+    auto old = std::min_element(m->graphs.begin(), m->graphs.end(),
+                                [](const dsi_model::Graph& x, const dsi_model::Graph& y) {
+                                  return x.used < y.used;
+                                });
+    hipGraphExecDestroy(old->exec);
+    m->graphs.erase(old);
+  }
+  m->graphs.push_back(dsi_model::Graph{key, exec, m->graph_clock});
+  HIP_TRY(hipGraphLaunch(exec, m->stream));
+  return DSI_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -487,6 +547,9 @@ dsi_status dsi_model_create(const dsi_config* cfg, void* stream, dsi_model** out
   if (!m) return fail(DSI_ENOMEM, "host allocation failed");
   m->cfg = c;
   m->stream = (hipStream_t)stream;
+  // graph replay needs a capturable stream (not the null stream)
+  const char* g = getenv("DSI_GRAPHS");
+  m->use_graphs = stream != nullptr && !(g && g[0] == '0');
   m->wtype = c.wdtype == DSI_BF16 ? W_BF16 : W_F32;
   m->kvb = c.kvdtype == DSI_BF16 ? 1 : 0;
   m->esz = m->wtype == W_BF16 ? 2 : 4;
@@ -553,6 +616,7 @@ dsi_status dsi_model_destroy(dsi_model* m) {
   if (!m) return DSI_OK;
   if (m->live_kv) return fail(DSI_ESTATE, "destroy the model's KV caches first");
   hipStreamSynchronize(m->stream);
+  for (auto& g : m->graphs) hipGraphExecDestroy(g.exec);
   for (hipEvent_t e : m->prof_ev) hipEventDestroy(e);
   free_list(m->allocs);
   if (m->attn_o.p) hipFree(m->attn_o.p);
@@ -689,7 +753,9 @@ dsi_status dsi_prefill(dsi_model* m, dsi_kv* kv, int32_t window, const int32_t* 
   for (int off = 0; off < n; off += kMaxRows) {
     const int rows = std::min(kMaxRows, n - off);
     const bool last = off + rows == n;
-    DSI_TRY(run_forward(m, kv, window, 1, rows, d_tokens + off, last ? d_last_logits : nullptr, 1,
+    AttnPlan ap;
+    DSI_TRY(plan_attention(m, kv, window, 1, rows, &ap));
+    DSI_TRY(run_forward(m, kv, ap, window, 1, rows, d_tokens + off, last ? d_last_logits : nullptr, 1,
                         nullptr));
     HIP_TRY(launch_kv_add_checked(kv->lens, window, d_tokens + off, rows, m->V, m->err, m->stream));
     kv->hi[window] += rows;
@@ -712,7 +778,8 @@ dsi_status dsi_verify(dsi_model* m, dsi_kv* kv, const dsi_verify_args* a, int32_
       return fail(DSI_ECAPACITY, "window %d: length (<= %lld) + %d exceeds max_len %d", a->window0 + b,
                   kv->hi[a->window0 + b], k + 1, kv->max_len);
   float* logits = a->d_logits_out ? a->d_logits_out : m->logits;
-  DSI_TRY(run_forward(m, kv, a->window0, B, k + 1, a->d_tokens, logits, 0, a->d_hidden_out));
+  AttnPlan ap;
+  DSI_TRY(plan_attention(m, kv, a->window0, B, k + 1, &ap));
   m->last_window0 = a->window0;
   m->last_B = B;
   m->last_R = k + 1;
@@ -733,9 +800,29 @@ dsi_status dsi_verify(dsi_model* m, dsi_kv* kv, const dsi_verify_args* a, int32_
   va.tok_out = d_next_token;
   va.err = m->err;
   verify_bind_workspace(va, m->vws, B * (k + 1), B, m->V);
-  {
+  auto launches = [&]() -> dsi_status {
+    DSI_TRY(run_forward(m, kv, ap, a->window0, B, k + 1, a->d_tokens, logits, 0, a->d_hidden_out));
     Prof p(m, DSI_K_VERIFY);
     HIP_TRY(launch_verify(va, m->stream));
+    return DSI_OK;
+  };
+  if (m->use_graphs && m->prof_class == 0) {
+    // every value the launches depend on (model-owned buffers are fixed for
+    // the model's lifetime except the attention partials, which are keyed)
+    uint32_t tbits;
+    memcpy(&tbits, &a->temperature, 4);
+    const std::vector<uint64_t> key = {
+        (uint64_t)a->window0, (uint64_t)B, (uint64_t)k, (uint64_t)(uintptr_t)a->d_tokens,
+        (uint64_t)(uintptr_t)a->d_q, (uint64_t)(uintptr_t)a->d_u, tbits, (uint64_t)a->mode,
+        (uint64_t)a->commit, (uint64_t)(uintptr_t)logits, (uint64_t)(uintptr_t)a->d_hidden_out,
+        (uint64_t)(uintptr_t)d_n_accepted, (uint64_t)(uintptr_t)d_next_token,
+        (uint64_t)(uintptr_t)kv->k, (uint64_t)(uintptr_t)kv->v, (uint64_t)(uintptr_t)kv->lens,
+        (uint64_t)kv->n_windows, (uint64_t)kv->max_len, (uint64_t)kv->maxlen_pad,
+        (uint64_t)ap.n_qtiles, (uint64_t)ap.chunk, (uint64_t)ap.n_chunks,
+        (uint64_t)(uintptr_t)m->attn_o.p, (uint64_t)(uintptr_t)m->attn_ml.p};
+    DSI_TRY(replay_or_capture(m, key, launches));
+  } else {
+    DSI_TRY(launches());
   }
   if (a->commit)
     for (int b = 0; b < B; ++b) kv->hi[a->window0 + b] += k + 1;

@@ -8,7 +8,8 @@
 // n_kv query heads times R window rows form the query side; they are cut
 // into tiles of 16 queries.  Per 32-key step a wavefront computes
 //   S^T[key][query] = K . Q^T     (A = 16 K rows, B = Q^T hi/lo)
-//   O^T[d][query]  += V^T . P^T   (A = V^T rows of the transposed cache)
+//   O^T[d][query]  += V^T . P^T   (A = V^T rows of the blocked, transposed
+//                                  value cache: 8 contiguous KB per step)
 // with 16x16x32 bf16 MFMAs (two per product for the hi/lo query or
 // probability split), so every operand is a 16-byte lane load and the
 // query owned by a lane (l % 16) is the same in S^T, P^T and O^T: the
@@ -24,7 +25,10 @@ namespace dsi {
 
 namespace {
 
-template <int KVB, int HD>
+// PIPE: each wave handles several 32-key steps (long prefixes); the loads
+// of its next step are issued as soon as the current step's K (after S) and
+// V (after O) fragments have been consumed, so they overlap the math.
+template <int KVB, int HD, int PIPE>
 __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
   constexpr int NWV = kAttnWaves;
   constexpr int DS = HD / 32;
@@ -90,10 +94,9 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
   const int r16 = lane & 15;
   const int kgrp = (lane >> 4) * 8;
 
-  for (int p0 = c0 + 32 * w; p0 < c1; p0 += 32 * NWV) {
-    // issue every K and V load of this 32-key step before any math
-    u32x4 kb16[2][DS], vb16[DT];
-    F8 kf32[2][DS], vf32[DT];
+  u32x4 kb16[2][DS], vb16[DT];
+  F8 kf32[2][DS], vf32[DT];
+  auto load_k = [&](int p0) {
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
       const int key = p0 + (r16 >> 2) * 8 + t * 4 + (r16 & 3);
@@ -108,15 +111,33 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
         }
       }
     }
+  };
+  auto load_v = [&](int p0) {
 #pragma unroll
     for (int t = 0; t < DT; ++t) {
-      const size_t vidx = vbase + (size_t)(t * 16 + r16) * a.maxlen + p0 + kgrp;
+      // 32-key block p0/32 of the blocked V^T cache: dims x 32 keys, contiguous
+      const size_t vidx = vbase + ((size_t)(p0 >> 5) * HD + t * 16 + r16) * 32 + kgrp;
       if (KVB) {
         vb16[t] = *(const u32x4*)((const uint16_t*)a.vc + vidx);
       } else {
         vf32[t].a = *(const float4*)((const float*)a.vc + vidx);
         vf32[t].b = *(const float4*)((const float*)a.vc + vidx + 4);
       }
+    }
+  };
+  if constexpr (PIPE) {
+    if (c0 + 32 * w < c1) {
+      load_k(c0 + 32 * w);
+      load_v(c0 + 32 * w);
+    }
+  }
+
+  for (int p0 = c0 + 32 * w; p0 < c1; p0 += 32 * NWV) {
+    const int pn = p0 + 32 * NWV;   // this wave's next step
+    if constexpr (!PIPE) {
+      // issue every K and V load of this 32-key step before any math
+      load_k(p0);
+      load_v(p0);
     }
     f32x4 st[2];
 #pragma unroll
@@ -133,6 +154,9 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
           for (int e = 0; e < 8; ++e) st[t] = mfma_f32(f8_get(kf32[t][ds], e), f8_get(qf[ds], e), st[t]);
         }
       }
+    }
+    if constexpr (PIPE) {
+      if (pn < c1) load_k(pn);
     }
     // lane holds keys p0 + kgrp + (t*4 + j) for query (lane & 15)
     float sv[8];
@@ -184,6 +208,9 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
       for (int t = 0; t < DT; ++t)
 #pragma unroll
         for (int e = 0; e < 8; ++e) o[t] = mfma_f32(f8_get(vf32[t], e), pv[e], o[t]);
+    }
+    if constexpr (PIPE) {
+      if (pn < c1) load_v(pn);
     }
   }
 
@@ -283,7 +310,10 @@ __global__ __launch_bounds__(128) void k_attn_combine(AttnArgs a) {
 template <int KVB, int HD>
 hipError_t launch_hd(const AttnArgs& a, hipStream_t s) {
   dim3 g1(a.n_chunks, a.n_qtiles, a.n_windows * a.n_kv);
-  hipLaunchKernelGGL((k_attn<KVB, HD>), g1, dim3(kAttnWaves * 64), 0, s, a);
+  if (a.chunk > kAttnChunkQuantum)
+    hipLaunchKernelGGL((k_attn<KVB, HD, 1>), g1, dim3(kAttnWaves * 64), 0, s, a);
+  else
+    hipLaunchKernelGGL((k_attn<KVB, HD, 0>), g1, dim3(kAttnWaves * 64), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   dim3 g2(HD / 32, a.n_qtiles, a.n_windows * a.n_kv);

@@ -200,7 +200,8 @@ __global__ void k_kv_add_checked(int* lens, int window, const int* tokens, int n
   }
 }
 
-// copy [n_kv][len][hd] <-> cache (K [n_kv][maxlen][hd], V^T [n_kv][hd][maxlen])
+// copy [n_kv][len][hd] <-> cache (K [n_kv][maxlen][hd], blocked V^T
+// [n_kv][maxlen/32][hd][32])
 template <typename T>
 __global__ void k_kv_copy(int to_cache, T* kc, T* vc, int n_kv, int hd, int maxlen, int len,
                           T* dk, T* dv) {
@@ -211,7 +212,7 @@ __global__ void k_kv_copy(int to_cache, T* kc, T* vc, int n_kv, int hd, int maxl
     const int p = (int)((i / hd) % len);
     const int h = (int)(i / ((size_t)hd * len));
     const size_t ki = ((size_t)h * maxlen + p) * hd + dd;
-    const size_t vi = ((size_t)h * hd + dd) * maxlen + p;
+    const size_t vi = (((size_t)h * (maxlen >> 5) + (p >> 5)) * hd + dd) * 32 + (p & 31);
     if (to_cache) {
       kc[ki] = dk[i];
       vc[vi] = dv[i];

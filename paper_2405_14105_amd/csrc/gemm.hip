@@ -117,7 +117,8 @@ __device__ __forceinline__ float epilogue(const EpiArgs& e, int nb, int r0, int 
         for (int j = 0; j < 4; ++j) {
           const int n = vb * 16 + r0 + j;
           const int h = n / hd, dd = n % hd;
-          const size_t idx = (((size_t)win * e.n_kv + h) * hd + dd) * e.maxlen + pos;
+          const size_t idx = ((((size_t)win * e.n_kv + h) * (e.maxlen >> 5) + (pos >> 5)) * hd + dd) * 32 +
+                             (pos & 31);
           if (e.kv_bf16) ((uint16_t*)e.vcache)[idx] = f2bf_bits(s[j]);
           else ((float*)e.vcache)[idx] = s[j];
         }
@@ -158,9 +159,11 @@ __device__ __forceinline__ void row_scales(const GemmArgs& a, float* rs) {
 
 // rs: per-row RMSNorm scales (row_scales) or nullptr.  The iteration count
 // is uniform across a wave, so the EPI_RESID lane reduction is safe.
+// NBW here is the number of n-blocks of one reduction round (red holds
+// NW x NBW x MT tiles); n-blocks j >= nvalid of the round are skipped.
 template <int WT, int EPI, int MT, int NBW, int NW>
 __device__ __forceinline__ void finish(const GemmArgs& a, const f32x4* red, const float* rs, int nb0,
-                                       int split, const ResidIn& pre) {
+                                       int nvalid, int split, const ResidIn& pre) {
   constexpr int ACC = NBW * MT;
   for (int it = threadIdx.x; it < ACC * 64; it += NW * 64) {
     const int l = it & 63, jm = it >> 6;
@@ -168,7 +171,7 @@ __device__ __forceinline__ void finish(const GemmArgs& a, const f32x4* red, cons
     f32x4 v = red[jm * 64 + l];
     for (int ww = 1; ww < NW; ++ww) v += red[(ww * ACC + jm) * 64 + l];
     const int nb = nb0 + j, m = t * 16 + (l & 15);
-    const bool ok = nb < a.Nb && m < a.M;
+    const bool ok = j < nvalid && nb < a.Nb && m < a.M;
     if (ok && rs) v *= rs[m];
     float sq = 0.f;
     if (ok) sq = epilogue<WT, EPI>(a.epi, nb, (l >> 4) * 4, m, split, v, pre);
@@ -201,10 +204,19 @@ __device__ __forceinline__ Work work_of(const GemmArgs& a) {
   return w;
 }
 
+// n-blocks per LDS reduction round: all of them when NW x NBW x MT tiles
+// (1 KB each) fit in kRedTiles KB, else as many as fit (several rounds)
+constexpr int kRedTiles = 128;
+template <int MT, int NBW, int NW>
+constexpr int red_nb() {
+  return NW * NBW * MT <= kRedTiles ? NBW : (kRedTiles / (NW * MT) > 0 ? kRedTiles / (NW * MT) : 1);
+}
+
 template <int MT, int NBW, int NW, int U, int EPI>
 __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(GemmArgs a) {
-  constexpr int ACC = NBW * MT;
-  __shared__ f32x4 red[NW * ACC * 64];
+  constexpr int NBR = red_nb<MT, NBW, NW>();
+  static_assert(EPI != EPI_RESID || NBR == NBW, "EPI_RESID reduces in one round");
+  __shared__ f32x4 red[NW * NBR * MT * 64];
   __shared__ float rs[kMaxRows];
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
@@ -265,11 +277,17 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(GemmArgs a) {
   }
 
 #pragma unroll
-  for (int j = 0; j < NBW; ++j)
+  for (int j0 = 0; j0 < NBW; j0 += NBR) {
+    if (j0 > 0) __syncthreads();   // the previous round's tiles have been read
 #pragma unroll
-    for (int t = 0; t < MT; ++t) red[((w * NBW + j) * MT + t) * 64 + lane] = acc[j][t];
-  __syncthreads();
-  finish<W_BF16, EPI, MT, NBW, NW>(a, red, a.ssq ? rs : nullptr, nb0, wk.split, pre);
+    for (int jj = 0; jj < NBR; ++jj)
+#pragma unroll
+      for (int t = 0; t < MT; ++t)
+        if (j0 + jj < NBW) red[((w * NBR + jj) * MT + t) * 64 + lane] = acc[j0 + jj][t];
+    __syncthreads();
+    finish<W_BF16, EPI, MT, NBR, NW>(a, red, a.ssq ? rs : nullptr, nb0 + j0, min(NBR, NBW - j0),
+                                     wk.split, pre);
+  }
 }
 
 template <int MT, int NBW, int NW, int EPI>
@@ -323,7 +341,7 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_f32(GemmArgs a) {
 #pragma unroll
     for (int t = 0; t < MT; ++t) red[((w * NBW + j) * MT + t) * 64 + lane] = acc[j][t];
   __syncthreads();
-  finish<W_F32, EPI, MT, NBW, NW>(a, red, a.ssq ? rs : nullptr, nb0, wk.split, pre);
+  finish<W_F32, EPI, MT, NBW, NW>(a, red, a.ssq ? rs : nullptr, nb0, NBW, wk.split, pre);
 }
 
 // Grid shaping.  Each wave reuses every activation fragment it loads across

@@ -34,8 +34,11 @@ namespace dsi {
 //    feature 8*nb + 2g + (jj & 1), gate for jj < 2 and up for jj >= 2.
 //
 // KV cache of one layer and window: K [n_kv][max_len_pad][hd] and the value
-// cache transposed, V^T [n_kv][hd][max_len_pad], so that both attention
-// MFMAs read 16 contiguous bytes per lane.
+// cache transposed in blocks of 32 positions, V^T [n_kv][max_len_pad/32][hd][32]
+// (max_len_pad is a multiple of 64).  Both attention MFMAs read 16
+// contiguous bytes per lane, and the keys and values of one 32-key step are
+// two contiguous blocks (32 x hd elements each), which keeps long-prefix
+// attention on long DRAM bursts.
 
 enum WType : int { W_F32 = 0, W_BF16 = 1 };
 

@@ -325,7 +325,9 @@ dsi_status plan_attention(dsi_model* m, dsi_kv* kv, int window0, int B, int R, A
   // therefore its results are identical alone or inside a batch.
   const int G = m->hq / m->hkv;
   p->n_qtiles = cdiv(G * R, 16);
-  const int want = std::max(1, cdiv(512, m->hkv * p->n_qtiles));
+  // about two workgroups per CU for one window (a full second round, not a
+  // short tail): at most 512 / (KV heads x query tiles) chunks
+  const int want = std::max(1, 512 / (m->hkv * p->n_qtiles));
   int chunk = (int)round_up((size_t)cdiv(kv->max_len, want), kAttnChunkQuantum);
   p->chunk = std::min(std::max(chunk, kAttnChunkQuantum), 16384);
   p->n_chunks = (int)((kmax + p->chunk - 1) / p->chunk);

@@ -57,38 +57,6 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
   const int mtok = win * R + ri;
   const int head = kvh * G + gh;
 
-  // query fragments (B operand of S^T): Q[q][ds*32 + 8*(l/16) + e]
-  const float* qrow = a.q + (size_t)mtok * (a.n_heads * HD) + head * HD;
-  bf16x8 qh[DS], ql[DS];
-  F8 qf[DS];
-#pragma unroll
-  for (int ds = 0; ds < DS; ++ds) {
-    const int d0 = ds * 32 + (lane >> 4) * 8;
-    F8 v;
-    if (qvalid) {
-      v.a = *(const float4*)(qrow + d0);
-      v.b = *(const float4*)(qrow + d0 + 4);
-    } else {
-      v.a = v.b = float4{0.f, 0.f, 0.f, 0.f};
-    }
-    if (KVB) {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        uint16_t h, l2;
-        split_bf16(f8_get(v, e), h, l2);
-        qh[ds][e] = __builtin_bit_cast(__bf16, h);
-        ql[ds][e] = __builtin_bit_cast(__bf16, l2);
-      }
-    } else {
-      qf[ds] = v;
-    }
-  }
-
-  float mrun = -INFINITY, lrun = 0.f;
-  f32x4 o[DT];
-#pragma unroll
-  for (int t = 0; t < DT; ++t) o[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-
   const size_t kbase = ((size_t)wabs * a.n_kv + kvh) * (size_t)a.maxlen * HD;
   const size_t vbase = ((size_t)wabs * a.n_kv + kvh) * (size_t)HD * a.maxlen;
   const int r16 = lane & 15;
@@ -125,19 +93,52 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
       }
     }
   };
-  if constexpr (PIPE) {
-    if (c0 + 32 * w < c1) {
-      load_k(c0 + 32 * w);
-      load_v(c0 + 32 * w);
+  // query (B operand of S^T): Q[q][ds*32 + 8*(l/16) + e].  Its loads are
+  // issued first, then the first step's K and V loads, and the query is
+  // split into hi/lo while those are in flight.
+  const float* qrow = a.q + (size_t)mtok * (a.n_heads * HD) + head * HD;
+  F8 qf[DS];
+#pragma unroll
+  for (int ds = 0; ds < DS; ++ds) {
+    const int d0 = ds * 32 + (lane >> 4) * 8;
+    if (qvalid) {
+      qf[ds].a = *(const float4*)(qrow + d0);
+      qf[ds].b = *(const float4*)(qrow + d0 + 4);
+    } else {
+      qf[ds].a = qf[ds].b = float4{0.f, 0.f, 0.f, 0.f};
     }
   }
+  const int pfirst = c0 + 32 * w;
+  if (pfirst < c1) {
+    load_k(pfirst);
+    load_v(pfirst);
+  }
+  bf16x8 qh[DS], ql[DS];
+  if (KVB) {
+#pragma unroll
+    for (int ds = 0; ds < DS; ++ds)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        uint16_t h, l2;
+        split_bf16(f8_get(qf[ds], e), h, l2);
+        qh[ds][e] = __builtin_bit_cast(__bf16, h);
+        ql[ds][e] = __builtin_bit_cast(__bf16, l2);
+      }
+  }
 
-  for (int p0 = c0 + 32 * w; p0 < c1; p0 += 32 * NWV) {
+  float mrun = -INFINITY, lrun = 0.f;
+  f32x4 o[DT];
+#pragma unroll
+  for (int t = 0; t < DT; ++t) o[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int p0 = pfirst; p0 < c1; p0 += 32 * NWV) {
     const int pn = p0 + 32 * NWV;   // this wave's next step
     if constexpr (!PIPE) {
-      // issue every K and V load of this 32-key step before any math
-      load_k(p0);
-      load_v(p0);
+      // later steps: every K and V load of the step before any math
+      if (p0 != pfirst) {
+        load_k(p0);
+        load_v(p0);
+      }
     }
     f32x4 st[2];
 #pragma unroll

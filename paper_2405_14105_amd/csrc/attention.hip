@@ -39,7 +39,15 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
 
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
-  const int c = blockIdx.x, y = blockIdx.y, z = blockIdx.z;
+  // XCD-aware order: workgroups are dispatched to the 8 XCDs round-robin by
+  // linear id, so ids 8 r + x land on XCD x.  The query tiles of one (chunk,
+  // window, KV head) unit u get ids congruent to u mod 8 -- the same XCD and
+  // L2 -- and read that unit's keys and values from HBM once.
+  const int xcd = blockIdx.x & 7, rr = blockIdx.x >> 3;
+  const int y = rr % a.n_qtiles;
+  const int u = (rr / a.n_qtiles) * 8 + xcd;
+  if (u >= a.n_chunks * a.n_windows * a.n_kv) return;
+  const int c = u % a.n_chunks, z = u / a.n_chunks;
   const int win = z / a.n_kv, kvh = z % a.n_kv;
   const int G = a.n_heads / a.n_kv;
   const int R = a.rows.rows_per_window;
@@ -310,7 +318,8 @@ __global__ __launch_bounds__(128) void k_attn_combine(AttnArgs a) {
 
 template <int KVB, int HD>
 hipError_t launch_hd(const AttnArgs& a, hipStream_t s) {
-  dim3 g1(a.n_chunks, a.n_qtiles, a.n_windows * a.n_kv);
+  const int units = a.n_chunks * a.n_windows * a.n_kv;
+  dim3 g1(((units + 7) / 8) * 8 * a.n_qtiles);
   if (a.chunk > kAttnChunkQuantum)
     hipLaunchKernelGGL((k_attn<KVB, HD, 1>), g1, dim3(kAttnWaves * 64), 0, s, a);
   else

@@ -29,11 +29,11 @@ import dsi_synth as S  # noqa: E402
 
 METRIC = "verify-step latency (ms) + verified draft tokens/s, 8B-shape k=10; % HBM peak"
 # HBM bytes per launch of the 8B gate/up kernel from the two counter runs in
-# profiles/gateup_8b_k10_pmc_traffic.md (FETCH_SIZE x 2.0 + WRITE_SIZE x 1.0,
+# profiles/verify_8b_k10_hbm_traffic.md (FETCH_SIZE x 2.0 + WRITE_SIZE x 1.0,
 # scales from a 512 MiB copy).  Reported only while the GEMM sources are the
 # ones the counters were taken with.
-TRAFFIC_MEASURED = {"workload": "llama8b_L2048_k10", "bytes": 237.73e6,
-                    "sources_sha256": "a1d1094f6bc698b4fda1629a8595368838f3f10238bd36913010a58bd1f4fe9e"}
+TRAFFIC_MEASURED = {"workload": "llama8b_L2048_k10", "bytes": 237.83e6,
+                    "sources_sha256": "39401ec5b0de6563fc74160e082646b5cebd18659bb29267707c261d89a90084"}
 GEMM_SOURCES = ("paper_2405_14105_amd/csrc/gemm.hip", "paper_2405_14105_amd/csrc/device_util.h",
                 "paper_2405_14105_amd/csrc/internal.h")
 HBM_PEAK_GBS = 8000.0
@@ -174,6 +174,7 @@ def run_gpu(args, wl):
         evs[i].record()
         step()
     evs[-1].record()
+    enqueue = time.time() - wall0   # host time to issue the calls (they are asynchronous)
     torch.cuda.synchronize()
     wall = time.time() - wall0
     per = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)])
@@ -209,7 +210,8 @@ def run_gpu(args, wl):
         log(f"{name} GEMM alone: {nl} launches, {avg * 1e3:.2f} us each")
     dsi.dsi_kv_destroy(kv)
     dsi.dsi_model_destroy(model)
-    return {"ms": ms, "per_step": per, "kernels": kt, "n_accepted": n_acc.tolist()}
+    return {"ms": ms, "per_step": per, "kernels": kt, "n_accepted": n_acc.tolist(),
+            "host_us_per_call": enqueue / args.steps * 1e6}
 
 
 # ------------------------------------------------------------ CPU baseline
@@ -280,8 +282,8 @@ def cpu_baseline(wl, sample_layers: int):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="llama8b_L2048_k10", choices=sorted(S.WORKLOADS))
     ap.add_argument("--mode", default="sample", choices=["sample", "greedy"])
     ap.add_argument("--cpu-sample-layers", type=int, default=2)
@@ -335,6 +337,8 @@ def main():
                    "head_dim": wl.shape.head_dim, "d_ff": wl.shape.d_ff, "vocab": wl.shape.vocab,
                    "prefix": list(wl.prefix_lens), "k": k, "windows": B, "mode": args.mode,
                    "temperature": wl.temperature},
+        "accepted_tokens_per_s": round(sum(n + 1 for n in g["n_accepted"]) / (ms * 1e-3), 1),
+        "host_us_per_call": round(g["host_us_per_call"], 1),   # dsi_verify + rollbacks, enqueue only
         "latency_ms": {"p10": round(float(np.percentile(g["per_step"], 10)), 4),
                        "p50": round(float(np.percentile(g["per_step"], 50)), 4),
                        "p90": round(float(np.percentile(g["per_step"], 90)), 4)},

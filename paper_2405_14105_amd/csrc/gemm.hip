@@ -404,7 +404,11 @@ template <int MT, int EPI>
 hipError_t launch_bf16(const GemmArgs& a, hipStream_t s) {
   constexpr int NW = Role<EPI>::NW, U = Role<EPI>::U;
   if constexpr (MT >= 2) {
-    return launch_bf16_cfg<MT, EPI, 2, NW, (U < 2 ? U : 2)>(a, s);
+    // several row tiles: fewer n-blocks per wave (registers), except the
+    // wide gate/up and LM-head outputs
+    if constexpr (EPI == EPI_SILU) return launch_bf16_cfg<MT, EPI, 4, NW, 1>(a, s);
+    else if constexpr (EPI == EPI_STORE) return launch_bf16_cfg<MT, EPI, 8, NW, 1>(a, s);
+    else return launch_bf16_cfg<MT, EPI, 2, NW, (U < 2 ? U : 2)>(a, s);
   } else if constexpr (EPI == EPI_QKV) {
     return launch_bf16_cfg<MT, EPI, 2, NW, U>(a, s);
   } else if constexpr (EPI == EPI_PART) {

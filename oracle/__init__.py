@@ -3,7 +3,9 @@
 A plain, slow, fp64 CPU statement of what the verification step computes:
 the target forward over a window of k drafted tokens against a cached prefix
 (``forward64``) and the lossless accept/reject of those drafts (``verify64``),
-plus exact enumerations that pin the accept/reject rule (``bruteforce``).
+plus exact enumerations that pin the accept/reject rule (``bruteforce``), and
+the drafter side of a speculative-inference iteration with the loop built
+from both (``drafting``: ``draft64``, ``si_loop64``).
 
 Only the tests, the smoke check and the CPU-baseline leg of the benchmark may
 import this package.  It shares no code with the HIP path and imports nothing
@@ -19,9 +21,11 @@ from .model import (bf16_round64, rmsnorm64, rope64, attention64, silu64,
                         layer64, head64, forward64, embed64)
 from .verification import VerifyResult, softmax64, verify64, verify64_batch
 from . import bruteforce
+from .drafting import DraftResult, draft64, draft_q32, draw_inverse_cdf, si_loop64
 
 __all__ = [
     "bf16_round64", "rmsnorm64", "rope64", "attention64", "silu64", "layer64",
     "head64", "forward64", "embed64", "VerifyResult", "softmax64", "verify64",
-    "verify64_batch", "bruteforce",
+    "verify64_batch", "bruteforce", "DraftResult", "draft64", "draft_q32", "draw_inverse_cdf",
+    "si_loop64",
 ]

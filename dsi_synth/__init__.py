@@ -92,7 +92,14 @@ SHAPES = {
                         kvdtype="f32", gains="random"),
     "gqa_hd64": Shape("gqa_hd64", 3, 256, 8, 2, 64, 688, 2050, gains="random"),
     "mha_hd128": Shape("mha_hd128", 2, 256, 2, 2, 128, 520, 1536, gains="random"),
+    # drafters: small models sharing a target's vocabulary
+    "tiny_draft": Shape("tiny_draft", 1, 64, 2, 2, 32, 128, 1024, wdtype="f32", kvdtype="f32"),
+    "ragged_draft": Shape("ragged_draft", 1, 96, 3, 1, 32, 200, 1003, gains="random"),
+    "llama8b_draft": Shape("llama8b_draft", 2, 1024, 16, 4, 64, 2816, 128256),
 }
+# the drafter paired with each target shape (same vocabulary)
+DRAFTERS = {"tiny": "tiny_draft", "ragged_bf16": "ragged_draft", "llama8b": "llama8b_draft"}
+DRAFT_SEED_OFFSET = 1000   # drafter weights: seed + this, independent of the target's
 
 WORKLOADS = {
     "tiny_k5": Workload("tiny_k5", SHAPES["tiny"], (64,), 5),

@@ -160,6 +160,31 @@ typedef struct {
 dsi_status dsi_verify(dsi_model* m, dsi_kv* kv, const dsi_verify_args* args,
                       int32_t* d_n_accepted, int32_t* d_next_token);
 
+/* Draft k tokens for one window with a drafter model that shares the
+ * target's vocabulary (Section 2: the drafter proposes the lookahead tokens
+ * one at a time, each sampled from its own next-token distribution given the
+ * context and the drafts before it).  The drafter's cache for `window` holds
+ * the context it has seen (length L_d).
+ *   d_feed [n_feed] int32: tokens the drafter has not seen yet, 1..DSI_MAX_ROWS
+ *            of them (the last committed token w0, preceded after a fully
+ *            accepted window by the last draft), cached at L_d ..
+ *   d_u    [k] fp32 in [0,1): one uniform per draft
+ *   temperature > 0
+ * Outputs (device): d_tokens [k+1] = (w0, d_1..d_k), the window dsi_verify
+ * takes; d_q [k][V] fp32, row i = the drafter distribution of d_{i+1}:
+ * softmax(z / temperature) computed in fp64 and stored in fp32, and d_{i+1}
+ * is drawn from that stored row by inverse CDF: the smallest t with
+ * sum_{v<=t} q_v > u_i * sum_v q_v (sums in fp64, ascending ids), else the
+ * last t with q_t > 0.  The drafter caches the feed and d_1..d_{k-1}: its
+ * length becomes L_d + n_feed + k - 1.  After the target accepts n drafts,
+ * roll the drafter back to keep w0, d_1..d_min(n, k-1) and feed the emitted
+ * token (preceded by d_k when n = k) to the next call.  Stream-ordered;
+ * feed ids outside [0, V) are reported by the next synchronising call
+ * (DSI_EINVAL) as for dsi_prefill. */
+dsi_status dsi_draft(dsi_model* drafter, dsi_kv* kv, int32_t window, const int32_t* d_feed,
+                     int32_t n_feed, int32_t k, const float* d_u, float temperature,
+                     int32_t* d_tokens, float* d_q);
+
 /* The accept/reject step alone, on caller-provided logits
  * d_logits [B*(k+1)][V] fp32 (window-major rows); other arguments as in
  * dsi_verify.  Uses a library workspace on the current device; calls that

@@ -190,6 +190,21 @@ struct VerifyArgs {
   int C;                // chunks per row
 };
 constexpr int kVerifyChunk = 4096;  // vocabulary entries per chunk (256 thr x 16)
+
+// drafter sampling (draft.hip): q = softmax(z / T) stored fp32 and one draft
+// drawn from it by inverse CDF
+struct DraftArgs {
+  const float* logits;  // [V] drafter logits of the row that ends the context
+  int V, C;
+  double temperature;
+  const float* u;       // [1] the uniform of this draft
+  float* q_out;         // [V] the stored distribution
+  int* tok_out;         // [1] the draft
+  double2* part;        // workspace [C]: chunk (max z/T, sum exp)
+  double* csum;         // workspace [C]: chunk sums of the stored q
+};
+size_t draft_workspace_bytes(int V);
+hipError_t launch_draft_sample(DraftArgs a, void* ws, hipStream_t s);
 size_t verify_workspace_bytes(int rows, int B, int V);
 void verify_bind_workspace(VerifyArgs& a, void* ws, int rows, int B, int V);
 hipError_t launch_verify(const VerifyArgs& a, hipStream_t s);

@@ -8,6 +8,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <cmath>
 #include <map>
 #include <mutex>
 #include <new>
@@ -105,6 +106,7 @@ struct dsi_model {
   float2* rope = nullptr;
   float* logits = nullptr;
   void* vws = nullptr;
+  void* dws = nullptr;          // drafter-sampling workspace
   int* err = nullptr;
   DevBuf attn_o, attn_ml;
   int live_kv = 0;
@@ -603,6 +605,7 @@ dsi_status dsi_model_create(const dsi_config* cfg, void* stream, dsi_model** out
   A((void**)&m->rope, (size_t)kMaxRows * (m->hd / 2) * sizeof(float2));
   A((void**)&m->logits, (size_t)kMaxRows * m->V * 4);
   A(&m->vws, verify_workspace_bytes(kMaxRows, kMaxRows, m->V));
+  A(&m->dws, draft_workspace_bytes(m->V));
 
   A((void**)&m->err, 64);
   if (st != DSI_OK) {
@@ -828,6 +831,44 @@ dsi_status dsi_verify(dsi_model* m, dsi_kv* kv, const dsi_verify_args* a, int32_
   }
   if (a->commit)
     for (int b = 0; b < B; ++b) kv->hi[a->window0 + b] += k + 1;
+  return DSI_OK;
+}
+
+dsi_status dsi_draft(dsi_model* m, dsi_kv* kv, int32_t window, const int32_t* d_feed, int32_t n_feed,
+                     int32_t k, const float* d_u, float temperature, int32_t* d_tokens, float* d_q) {
+  if (!m || !kv || kv->m != m) return fail(DSI_EINVAL, "model / kv mismatch");
+  if (window < 0 || window >= kv->n_windows) return fail(DSI_EINVAL, "bad window %d", window);
+  if (n_feed < 1 || n_feed > kMaxRows || !d_feed)
+    return fail(DSI_EINVAL, "feed 1..%d tokens (got %d)", kMaxRows, n_feed);
+  if (k < 1) return fail(DSI_EINVAL, "k must be >= 1");
+  if (!d_u || !d_tokens || !d_q) return fail(DSI_EINVAL, "null uniforms / output pointer");
+  if (!(temperature > 0.f) || !std::isfinite(temperature)) return fail(DSI_EINVAL, "temperature must be > 0");
+  if (!all_set(m)) return fail(DSI_ESTATE, "not every model tensor has been set");
+  if (kv->hi[window] + n_feed + k - 1 > kv->max_len)
+    return fail(DSI_ECAPACITY, "window %d: length (<= %lld) + %d exceeds max_len %d", window, kv->hi[window],
+                n_feed + k - 1, kv->max_len);
+  hipStream_t s = m->stream;
+  // w0, the last fed token, opens the verification window
+  HIP_TRY(hipMemcpyAsync(d_tokens, d_feed + n_feed - 1, sizeof(int32_t), hipMemcpyDeviceToDevice, s));
+  for (int i = 0; i < k; ++i) {
+    // step i forwards the unseen feed (i = 0) or the previous draft, whose
+    // last row's logits give q_{i+1} and d_{i+1}
+    const int* rows = i == 0 ? d_feed : d_tokens + i;
+    const int R = i == 0 ? n_feed : 1;
+    AttnPlan ap;
+    DSI_TRY(plan_attention(m, kv, window, 1, R, &ap));
+    DSI_TRY(run_forward(m, kv, ap, window, 1, R, rows, m->logits, 1, nullptr));
+    HIP_TRY(launch_kv_add_checked(kv->lens, window, rows, R, m->V, m->err, s));
+    kv->hi[window] += R;
+    DraftArgs da{};
+    da.logits = m->logits;
+    da.V = m->V;
+    da.temperature = (double)temperature;
+    da.u = d_u + i;
+    da.q_out = d_q + (size_t)i * m->V;
+    da.tok_out = d_tokens + i + 1;
+    HIP_TRY(launch_draft_sample(da, m->dws, s));
+  }
   return DSI_OK;
 }
 

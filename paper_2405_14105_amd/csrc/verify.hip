@@ -24,7 +24,7 @@
 #include <limits.h>
 #include <math.h>
 
-#include "device_util.h"
+#include "scan.h"
 
 namespace dsi {
 
@@ -32,22 +32,6 @@ namespace {
 
 constexpr int VT = 256;                  // threads per workgroup
 constexpr int PER = kVerifyChunk / VT;   // 16 entries per thread
-
-// inclusive block scan of one double per thread, fixed association
-__device__ double block_scan_incl(double v, double* sh) {
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const double t = __shfl_up(v, o);
-    if (lane >= o) v += t;
-  }
-  if (lane == 63) sh[w] = v;
-  __syncthreads();
-  double off = 0.0;
-  for (int i = 0; i < w; ++i) off += sh[i];
-  __syncthreads();
-  return off + v;
-}
 
 __global__ __launch_bounds__(VT) void k_vrow(VerifyArgs a) {
   __shared__ double shd[4];
@@ -206,8 +190,8 @@ __global__ __launch_bounds__(VT) void k_vresid(VerifyArgs a) {
       sp += draw_mass(a, zrow, qrow, st.x, st.y, false, v);
     }
   }
-  const double ir = block_scan_incl(sr, sh);
-  const double ip = block_scan_incl(sp, sh);
+  const double ir = block_scan_incl<VT / 64>(sr, sh);
+  const double ip = block_scan_incl<VT / 64>(sp, sh);
   if (threadIdx.x == VT - 1) a.csum[(size_t)b * a.C + c] = make_double2(ir, ip);
 }
 
@@ -280,7 +264,7 @@ __global__ __launch_bounds__(VT) void k_vsample(VerifyArgs a) {
     own += vals[i];
     if (vals[i] > 0.0) lastpos = v;
   }
-  const double incl = block_scan_incl(own, sh);
+  const double incl = block_scan_incl<VT / 64>(own, sh);
   // exclusive prefix of this thread = inclusive prefix of the previous one
   __shared__ double sincl[VT];
   sincl[threadIdx.x] = incl;

@@ -25,7 +25,7 @@ TENSOR_IDS = {
 }
 EXPORTED = (
     "dsi_model_create", "dsi_model_set_tensor", "dsi_model_destroy", "dsi_kv_create",
-    "dsi_kv_destroy", "dsi_prefill", "dsi_verify", "dsi_accept", "dsi_kv_rollback",
+    "dsi_kv_destroy", "dsi_prefill", "dsi_verify", "dsi_draft", "dsi_accept", "dsi_kv_rollback",
     "dsi_kv_length", "dsi_sync", "dsi_kv_export", "dsi_kv_import", "dsi_kv_set_length",
     "dsi_profile_begin", "dsi_profile_end", "dsi_profile_kernel", "dsi_last_error",
 )
@@ -77,6 +77,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "dsi_kv_destroy": ([P], I32),
         "dsi_prefill": ([P, P, I32, P, I32, P], I32),
         "dsi_verify": ([P, P, ctypes.POINTER(dsi_verify_args), P, P], I32),
+        "dsi_draft": ([P, P, I32, P, I32, I32, P, F, P, P], I32),
         "dsi_accept": ([P, I32, I32, I32, P, P, P, P, F, I32, P, P], I32),
         "dsi_kv_rollback": ([P, I32, I32], I32),
         "dsi_kv_length": ([P, I32, ctypes.POINTER(ctypes.c_int32)], I32),
@@ -151,6 +152,12 @@ def dsi_verify(model: int, kv: int, window0: int, n_windows: int, k: int, d_toke
     a = dsi_verify_args(window0, n_windows, k, _ptr(d_tokens), _ptr(d_q), _ptr(d_u), temperature,
                         mode, int(commit), _ptr(d_logits_out), _ptr(d_hidden_out))
     _check(load().dsi_verify(model, kv, ctypes.byref(a), _ptr(d_n_accepted), _ptr(d_next_token)))
+
+
+def dsi_draft(model: int, kv: int, window: int, d_feed, n_feed: int, k: int, d_u, d_tokens, d_q,
+              temperature: float = 1.0):
+    _check(load().dsi_draft(model, kv, window, _ptr(d_feed), n_feed, k, _ptr(d_u), temperature,
+                            _ptr(d_tokens), _ptr(d_q)))
 
 
 def dsi_accept(stream: int, n_windows: int, k: int, vocab: int, d_logits, d_tokens, d_q, d_u,

@@ -1,0 +1,191 @@
+"""On-device drafting (dsi_draft) and the speculative-inference loop on one
+GPU (draft with a small drafter, verify with the target, commit, roll the
+drafter back), against the oracle (oracle/drafting.py).
+
+Gates:
+  * draws: each draft equals the inverse-CDF draw from the GPU's own stored
+    q row with its uniform (split check), except within 1e-9 of a boundary;
+  * rows: the stored q rows match the oracle's rows for the same drafted
+    tokens (teacher forcing) within the logit tolerance: |ln q_gpu - ln q|
+    <= 2 delta with delta = 1e-4 (fp32 models) or 2e-2 (bf16);
+  * cache: the drafter's length grows by n_feed + k - 1;
+  * loop (fp32 models): every iteration's window, accepted count and token
+    equal the oracle loop's until the first iteration whose decisions lie
+    within the flag margins.
+"""
+import numpy as np
+import pytest
+import torch
+
+import dsi_synth as S
+from oracle import draft64, draw_inverse_cdf, forward64, si_loop64, verify64
+from paper_2405_14105_amd import dsi
+
+from gpu_rig import Rig
+from parity import TOL, getter
+
+pytestmark = pytest.mark.gpu
+
+SEED = 0
+DSEED = SEED + S.DRAFT_SEED_OFFSET
+
+
+def run_draft(rig, window, feed, k, u, temperature=1.0):
+    dev = rig.dev
+    f = rig.dev_i32(feed)
+    du = rig.dev_f32(u)
+    tok = torch.full((k + 1,), -7, dtype=torch.int32, device=dev)
+    q = torch.zeros((k, rig.shape.vocab), dtype=torch.float32, device=dev)
+    dsi.dsi_draft(rig.model, rig.kv, window, f, len(feed), k, du, tok, q, temperature)
+    torch.cuda.synchronize()
+    return tok.cpu().numpy(), q.cpu().numpy()
+
+
+@pytest.mark.parametrize("target,T", [("tiny", 1.0), ("ragged_bf16", 1.0), ("tiny", 0.7)])
+def test_draft_rows_and_draws(target, T):
+    ds = S.SHAPES[S.DRAFTERS[target]]
+    L, k = 40, 6
+    with Rig(ds, DSEED, 1, L + 2 * k + 4) as rig:
+        prefix = S.prefix_tokens(ds, SEED, 0, L)
+        rig.prefill(0, prefix)
+        rng = np.random.default_rng(7)
+        u = rng.random(k).astype(np.float32)
+        feed = [int(rng.integers(0, ds.vocab)), int(rng.integers(0, ds.vocab))]
+        tok, q = run_draft(rig, 0, feed, k, u, T)
+        assert rig.length(0) == L + len(feed) + k - 1
+    assert tok[0] == feed[-1]
+    # split check: every draft is the inverse-CDF draw from its own stored row
+    for i in range(k):
+        t, margin = draw_inverse_cdf(q[i], float(u[i]))
+        if margin >= 1e-9:
+            assert tok[i + 1] == t, i
+        assert abs(float(q[i].astype(np.float64).sum()) - 1.0) < 1e-4
+    # rows against the oracle drafter on the same drafted tokens
+    get = getter(ds, DSEED)
+    _, cache = forward64(ds, get, prefix)
+    ref = draft64(ds, get, cache, feed, k, u, T, forced=tok[1:])
+    delta = TOL[ds.wdtype]
+    lq, lr = np.log(np.maximum(q, 1e-30)), np.log(np.maximum(ref.q, 1e-30))
+    mask = ref.q > 1e-20
+    err = float(np.abs(lq - lr)[mask].max())
+    print(f"{target}: max |ln q_gpu - ln q_oracle| = {err:.3g}")
+    assert err <= 2 * delta + 1e-6
+
+
+def test_draft_input_errors():
+    ds = S.SHAPES["tiny_draft"]
+    with Rig(ds, DSEED, 1, 20) as rig:
+        rig.prefill(0, S.prefix_tokens(ds, SEED, 0, 10))
+        u = np.full(4, 0.5, np.float32)
+        with pytest.raises(dsi.DsiError) as ei:
+            run_draft(rig, 0, [3], 0, u)
+        assert ei.value.status == dsi.DSI_EINVAL
+        with pytest.raises(dsi.DsiError) as ei:     # 10 + 2 + 10 - 1 > 20
+            run_draft(rig, 0, [3, 4], 10, np.full(10, 0.5, np.float32))
+        assert ei.value.status == dsi.DSI_ECAPACITY
+        assert rig.length(0) == 10
+
+
+def gpu_si_loop(trig, drig, prefix_len, w0, k, ud, uv):
+    """The SI loop on the GPU: draft, verify (commit), roll the drafter back."""
+    V = trig.shape.vocab
+    out = []
+    feed = [int(w0)]
+    for it in range(len(ud)):
+        tok, q = run_draft(drig, 0, feed, k, ud[it])
+        res = trig.verify(0, tok[None, :], q[None], uv[it][None], commit=True)
+        n, t = int(res["n"][0]), int(res["token"][0])
+        out.append((tok.copy(), n, t, q, res["logits"]))
+        # drafter keeps w0, d_1..d_min(n, k-1); the target keeps w0, d_1..d_n
+        Lt = trig.length(0)
+        Ld = Lt - n - 1 + 1 + min(n, k - 1)
+        dsi.dsi_kv_rollback(drig.kv, 0, Ld)
+        feed = ([int(tok[k])] if n == k else []) + [t]
+    return out
+
+
+def test_si_loop_matches_oracle_fp32():
+    ts, ds = S.SHAPES["tiny"], S.SHAPES["tiny_draft"]
+    L, k, iters = 32, 4, 6
+    rng = np.random.default_rng(11)
+    ud = rng.random((iters, k)).astype(np.float32)
+    uv = rng.random((iters, k + 1)).astype(np.float32)
+    prefix = S.prefix_tokens(ts, SEED, 0, L)
+    w0 = 17
+    cap = L + iters * (k + 2) + 4
+    with Rig(ts, SEED, 1, cap) as trig, Rig(ds, DSEED, 1, cap) as drig:
+        trig.prefill(0, prefix)
+        drig.prefill(0, prefix)
+        got = gpu_si_loop(trig, drig, L, w0, k, ud, uv)
+    ref = si_loop64(ts, getter(ts, SEED), ds, getter(ds, DSEED), prefix, w0, k,
+                    ud.astype(np.float64), uv.astype(np.float64))
+    compared = 0
+    for it, ((tok, n, t, q, z), r) in enumerate(zip(got, ref)):
+        # the GPU's own decisions on its own rows (split check, always)
+        for i in range(k):
+            tt, margin = draw_inverse_cdf(q[i], float(ud[it][i]))
+            if margin >= 1e-9:
+                assert tok[i + 1] == tt, (it, i)
+        rv = verify64(z, tok[1:], q, uv[it])
+        if rv.accept_margin >= 1e-4 and rv.draw_margin >= 1e-9:
+            assert (n, t) == (rv.n, rv.token), it
+        # against the oracle loop while nothing was within the flag margins
+        if r.accept_margin < 1e-4 or r.draw_margin < 1e-6:
+            break
+        assert np.array_equal(tok, r.window), it
+        assert (n, t) == (r.n, r.token), it
+        compared += 1
+    print(f"SI loop: {compared} of {iters} iterations compared with the oracle loop")
+    assert compared >= 3
+
+
+def test_si_loop_split_checks_bf16():
+    ts, ds = S.SHAPES["ragged_bf16"], S.SHAPES["ragged_draft"]
+    L, k, iters = 24, 5, 5
+    rng = np.random.default_rng(12)
+    ud = rng.random((iters, k)).astype(np.float32)
+    uv = rng.random((iters, k + 1)).astype(np.float32)
+    prefix = S.prefix_tokens(ts, SEED, 0, L)
+    cap = L + iters * (k + 2) + 4
+    with Rig(ts, SEED, 1, cap) as trig, Rig(ds, DSEED, 1, cap) as drig:
+        trig.prefill(0, prefix)
+        drig.prefill(0, prefix)
+        got = gpu_si_loop(trig, drig, L, 5, k, ud, uv)
+        total = L
+        for it, (tok, n, t, q, z) in enumerate(got):
+            for i in range(k):
+                tt, margin = draw_inverse_cdf(q[i], float(ud[it][i]))
+                if margin >= 1e-9:
+                    assert tok[i + 1] == tt, (it, i)
+            rv = verify64(z, tok[1:], q, uv[it])
+            if rv.accept_margin >= 1e-4 and rv.draw_margin >= 1e-9:
+                assert (n, t) == (rv.n, rv.token), it
+            if it:
+                assert tok[0] == got[it - 1][2]
+            total += n + 1
+        assert trig.length(0) == total
+
+
+def test_si_loop_self_drafting_accepts_every_draft():
+    """Drafter = target (same weights): q = p up to fp32 rounding, so every
+    draft is accepted and each window carries the last draft into the next
+    feed (the n = k path of the drafter bookkeeping)."""
+    ts = S.SHAPES["tiny"]
+    L, k, iters = 20, 3, 4
+    rng = np.random.default_rng(13)
+    ud = rng.random((iters, k)).astype(np.float32)
+    uv = rng.random((iters, k + 1)).astype(np.float32)
+    prefix = S.prefix_tokens(ts, SEED, 0, L)
+    cap = L + iters * (k + 2) + 4
+    with Rig(ts, SEED, 1, cap) as trig, Rig(ts, SEED, 1, cap) as drig:
+        trig.prefill(0, prefix)
+        drig.prefill(0, prefix)
+        got = gpu_si_loop(trig, drig, L, 9, k, ud, uv)
+        assert trig.length(0) == L + iters * (k + 1)
+    ref = si_loop64(ts, getter(ts, SEED), ts, getter(ts, SEED), prefix, 9, k,
+                    ud.astype(np.float64), uv.astype(np.float64))
+    for it, ((tok, n, t, q, z), r) in enumerate(zip(got, ref)):
+        assert n == k, it
+        if r.draw_margin < 1e-6:
+            break
+        assert np.array_equal(tok, r.window) and (n, t) == (r.n, r.token), it

@@ -101,12 +101,12 @@ def measured_traffic(workload: str):
 
 
 # ------------------------------------------------------------------ GPU part
-def build_model(dsi, loader, shape, stream, n_windows, max_len):
+def build_model(dsi, loader, shape, stream, n_windows, max_len, seed=SEED):
     model = dsi.dsi_model_create(loader.config_for(shape), stream)
 
     def make(l, n):
-        return S.weight_bf16_bits(shape, SEED, l, n) if shape.wdtype == "bf16" else \
-            S.weight(shape, SEED, l, n)
+        return S.weight_bf16_bits(shape, seed, l, n) if shape.wdtype == "bf16" else \
+            S.weight(shape, seed, l, n)
 
     def progress(l):
         if (l + 1) % 8 == 0:
@@ -279,6 +279,79 @@ def cpu_baseline(wl, sample_layers: int):
     }
 
 
+def run_si(args, wl):
+    """The speculative-inference loop on one GPU: the workload's target and its
+    paired drafter (same vocabulary), k drafts per iteration, the drafter rolled
+    back after each verification.  Reports the per-iteration time split."""
+    import torch
+    from paper_2405_14105_amd import dsi, loader
+
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a GPU (cuda:0)")
+    dsi.load()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_stream(torch.cuda.Stream())
+    stream = torch.cuda.current_stream().cuda_stream
+    ts, k, L = wl.shape, wl.k, wl.prefix_lens[0]
+    ds = S.SHAPES[S.DRAFTERS[ts.name]]
+    iters = args.steps
+    cap = L + (args.warmup + iters) * (k + 2) + 8
+    target, tkv = build_model(dsi, loader, ts, stream, 1, cap)
+    drafter, dkv = build_model(dsi, loader, ds, stream, 1, cap, seed=SEED + S.DRAFT_SEED_OFFSET)
+    prefix = torch.from_numpy(S.prefix_tokens(ts, SEED, 0, L)).to(dev)
+    dsi.dsi_prefill(target, tkv, 0, prefix, L, None)
+    dsi.dsi_prefill(drafter, dkv, 0, prefix, L, None)
+    V = ts.vocab
+    feed = torch.zeros(2, dtype=torch.int32, device=dev)
+    tok = torch.zeros(k + 1, dtype=torch.int32, device=dev)
+    q = torch.zeros((k, V), dtype=torch.float32, device=dev)
+    ud = torch.zeros(k, dtype=torch.float32, device=dev)
+    uv = torch.zeros(k + 1, dtype=torch.float32, device=dev)
+    n_out = torch.zeros(1, dtype=torch.int32, device=dev)
+    t_out = torch.zeros(1, dtype=torch.int32, device=dev)
+    rng = np.random.default_rng(SEED)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    feed_host = [int(rng.integers(0, V))]
+    draft_ms, verify_ms, iter_ms, emitted = [], [], [], 0
+    for it in range(args.warmup + iters):
+        feed[:len(feed_host)].copy_(torch.tensor(feed_host, dtype=torch.int32))
+        ud.copy_(torch.from_numpy(rng.random(k).astype(np.float32)))
+        uv.copy_(torch.from_numpy(rng.random(k + 1).astype(np.float32)))
+        torch.cuda.synchronize()
+        t0 = time.time()
+        ev[0].record()
+        dsi.dsi_draft(drafter, dkv, 0, feed, len(feed_host), k, ud, tok, q, wl.temperature)
+        ev[1].record()
+        dsi.dsi_verify(target, tkv, 0, 1, k, tok, q, uv, n_out, t_out, wl.temperature,
+                       dsi.DSI_SAMPLE, True)
+        ev[2].record()
+        n, t = int(n_out.item()), int(t_out.item())   # the host needs n to roll the drafter back
+        Lt = dsi.dsi_kv_length(tkv, 0)
+        dsi.dsi_kv_rollback(dkv, 0, Lt - n - 1 + 1 + min(n, k - 1))
+        feed_host = ([int(tok[k].item())] if n == k else []) + [t]
+        wall = (time.time() - t0) * 1e3
+        if it >= args.warmup:
+            draft_ms.append(ev[0].elapsed_time(ev[1]))
+            verify_ms.append(ev[1].elapsed_time(ev[2]))
+            iter_ms.append(wall)
+            emitted += n + 1
+    dsi.dsi_sync(target)
+    dsi.dsi_sync(drafter)
+    total_s = sum(iter_ms) * 1e-3
+    out = {"metric": "speculative-inference loop on one GPU: emitted tokens/s",
+           "value": round(emitted / total_s, 1), "unit": "emitted tokens/s",
+           "iterations": iters, "warmup": args.warmup, "data": "synthetic",
+           "config": {"target": ts.name, "drafter": ds.name, "prefix": L, "k": k},
+           "draft_ms": round(float(np.mean(draft_ms)), 4),
+           "verify_ms": round(float(np.mean(verify_ms)), 4),
+           "iteration_ms": round(float(np.mean(iter_ms)), 4),
+           "mean_accepted": round(emitted / iters - 1, 3)}
+    for m, kv in ((target, tkv), (drafter, dkv)):
+        dsi.dsi_kv_destroy(kv)
+        dsi.dsi_model_destroy(m)
+    print(json.dumps(out))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -292,6 +365,8 @@ def main():
                     help="skip the per-class event timing pass (for counter runs)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one 512 MiB device copy first (counter scale reference)")
+    ap.add_argument("--si", action="store_true",
+                    help="time the draft + verify loop with the workload's drafter instead")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: this verification step is a single-GPU kernel path "
@@ -299,6 +374,9 @@ def main():
               f"windows on one GPU (workload llama8b_x7_L1024_k5).", file=sys.stderr)
         sys.exit(2)
     wl = S.WORKLOADS[args.workload]
+    if args.si:
+        run_si(args, wl)
+        return
     g = run_gpu(args, wl)
     sb = step_bytes(wl.shape, wl.prefix_lens, wl.k)
     ms = g["ms"]

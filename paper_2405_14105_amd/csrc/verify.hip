@@ -94,20 +94,25 @@ __global__ __launch_bounds__(VT) void k_vrow(VerifyArgs a) {
   }
 }
 
-// one wavefront per window
-__global__ __launch_bounds__(64) void k_vdecide(VerifyArgs a) {
-  const int b = blockIdx.x, lane = threadIdx.x;
+// one workgroup per window: each wave combines the chunk statistics of a
+// row (lanes over chunks, butterfly in fixed order), then wave 0 decides
+__global__ __launch_bounds__(VT) void k_vdecide(VerifyArgs a) {
+  __shared__ double sM[kMaxRows], sS[kMaxRows];
+  __shared__ int sArg[kMaxRows];
+  const int b = blockIdx.x, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int k = a.k, R = k + 1;
-  double M = -INFINITY, S = 0.0;
-  int arg = 0;
-  if (lane < R) {
-    const int r = b * R + lane;
-    for (int c = 0; c < a.C; ++c) M = fmax(M, a.part[(size_t)r * a.C + c].x);
+  for (int i = w; i < R; i += VT / 64) {
+    const int r = b * R + i;
+    double m = -INFINITY;
+    for (int c = lane; c < a.C; c += 64) m = fmax(m, a.part[(size_t)r * a.C + c].x);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) m = fmax(m, __shfl_xor(m, o));
+    double sum = 0.0;
     float bv = -INFINITY;
     int bi = INT_MAX;
-    for (int c = 0; c < a.C; ++c) {
+    for (int c = lane; c < a.C; c += 64) {
       const double2 pc = a.part[(size_t)r * a.C + c];
-      S += pc.y * exp(pc.x - M);
+      sum += pc.y * exp(pc.x - m);
       const float2 pa = a.part_arg[(size_t)r * a.C + c];
       const int ia = __float_as_int(pa.y);
       if (pa.x > bv || (pa.x == bv && ia < bi)) {
@@ -115,10 +120,29 @@ __global__ __launch_bounds__(64) void k_vdecide(VerifyArgs a) {
         bi = ia;
       }
     }
-    arg = bi;
-    a.rowstat[r] = make_double2(M, S);
-    a.rowarg[r] = arg;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      sum += __shfl_xor(sum, o);
+      const float ov = __shfl_xor(bv, o);
+      const int oi = __shfl_xor(bi, o);
+      if (ov > bv || (ov == bv && oi < bi)) {
+        bv = ov;
+        bi = oi;
+      }
+    }
+    if (lane == 0) {
+      sM[i] = m;
+      sS[i] = sum;
+      sArg[i] = bi;
+      a.rowstat[r] = make_double2(m, sum);
+      a.rowarg[r] = bi;
+    }
   }
+  __syncthreads();
+  if (w != 0) return;
+  const double M = lane < R ? sM[lane] : 0.0;
+  const double S = lane < R ? sS[lane] : 1.0;
+  const int arg = lane < R ? sArg[lane] : 0;
   int bad = 0;
   bool acc = true;
   if (lane < R) {
@@ -206,29 +230,48 @@ __global__ __launch_bounds__(VT) void k_vsample(VerifyArgs a) {
   const int n = dec.x, r = dec.y;
   const bool residual0 = dec.z != 0;
   const double2 st = a.rowstat[r];
-  if (threadIdx.x == 0) {
-    double R = 0.0;
-    for (int c = 0; c < a.C; ++c) R += a.csum[(size_t)b * a.C + c].x;
+  if (threadIdx.x < 64) {
+    // wave 0: prefix sums over the chunk sums, 64 chunks at a time, in one
+    // fixed order for the total and for locating the chunk
+    const int lane = threadIdx.x;
+    const int groups = (a.C + 63) / 64;
+    auto prefix = [&](int g, double carry, int usep) {
+      const int c = g * 64 + lane;
+      double x = 0.0;
+      if (c < a.C) {
+        const double2 cs = a.csum[(size_t)b * a.C + c];
+        x = usep ? cs.y : cs.x;
+      }
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const double t = __shfl_up(x, o);
+        if (lane >= o) x += t;
+      }
+      return carry + x;
+    };
     int usep = 0;
-    if (residual0 && !(R > 0.0)) {
+    double R = 0.0;
+    for (int g = 0; g < groups; ++g) R = __shfl(prefix(g, R, 0), 63);
+    if (residual0 && !(R > 0.0)) {   // no residual mass: draw from p
       usep = 1;
       R = 0.0;
-      for (int c = 0; c < a.C; ++c) R += a.csum[(size_t)b * a.C + c].y;
+      for (int g = 0; g < groups; ++g) R = __shfl(prefix(g, R, 1), 63);
     }
     const double target = (double)a.u[b * (a.k + 1) + a.k] * R;
-    double cum = 0.0;
     int chunk = -1;
-    double base = 0.0;
-    for (int c = 0; c < a.C; ++c) {
-      const double2 cs = a.csum[(size_t)b * a.C + c];
-      const double x = usep ? cs.y : cs.x;
-      const double nc = cum + x;
-      if (nc > target) {
-        chunk = c;
-        base = cum;
+    double base = 0.0, carry = 0.0;
+    for (int g = 0; g < groups; ++g) {
+      const double incl = prefix(g, carry, usep);
+      const double prev = __shfl_up(incl, 1);
+      const double excl = lane ? prev : carry;
+      const unsigned long long hit = __ballot(g * 64 + lane < a.C && incl > target);
+      if (hit) {   // uniform across the wave
+        const int l = __ffsll((long long)hit) - 1;
+        chunk = g * 64 + l;
+        base = __shfl(excl, l);
         break;
       }
-      cum = nc;
+      carry = __shfl(incl, 63);
     }
     int found = 1;
     if (chunk < 0) {               // rounding left no crossing: last chunk with mass
@@ -242,13 +285,15 @@ __global__ __launch_bounds__(VT) void k_vsample(VerifyArgs a) {
       }
       if (chunk < 0) chunk = a.C - 1;
     }
-    s_chunk = chunk;
-    s_base = base;
-    s_target = target;
-    s_usep = usep;
-    s_found = found;
-    s_first = INT_MAX;
-    s_last = -1;
+    if (lane == 0) {
+      s_chunk = chunk;
+      s_base = base;
+      s_target = target;
+      s_usep = usep;
+      s_found = found;
+      s_first = INT_MAX;
+      s_last = -1;
+    }
   }
   __syncthreads();
   const bool residual = residual0 && !s_usep;
@@ -328,7 +373,7 @@ void verify_bind_workspace(VerifyArgs& a, void* ws, int rows, int B, int V) {
 hipError_t launch_verify(const VerifyArgs& a, hipStream_t s) {
   const int rows = a.B * (a.k + 1);
   hipLaunchKernelGGL(k_vrow, dim3(a.C, rows), dim3(VT), 0, s, a);
-  hipLaunchKernelGGL(k_vdecide, dim3(a.B), dim3(64), 0, s, a);
+  hipLaunchKernelGGL(k_vdecide, dim3(a.B), dim3(VT), 0, s, a);
   if (!a.greedy) {
     hipLaunchKernelGGL(k_vresid, dim3(a.C, a.B), dim3(VT), 0, s, a);
     hipLaunchKernelGGL(k_vsample, dim3(a.B), dim3(VT), 0, s, a);

@@ -412,7 +412,7 @@ hipError_t launch_bf16(const GemmArgs& a, hipStream_t s) {
   } else if constexpr (EPI == EPI_QKV) {
     return launch_bf16_cfg<MT, EPI, 2, NW, U>(a, s);
   } else if constexpr (EPI == EPI_PART) {
-    return launch_bf16_cfg<MT, EPI, 4, NW, U>(a, s);
+    return launch_bf16_cfg<MT, EPI, 4, NW, 1>(a, s);
   } else if constexpr (EPI == EPI_RESID) {
     return launch_bf16_cfg<MT, EPI, 1, NW, U>(a, s);
   } else if constexpr (EPI == EPI_SILU) {

@@ -1,0 +1,53 @@
+"""Algorithm 1 over the library (paper_2405_14105_amd/executor.py): with
+exact-match verification DSI returns exactly the target's own greedy tokens
+(Theorem 1: the same output as the target alone), whatever the drafter, the
+lookahead and the number of target servers; and its simulated wall time is
+never above non-SI's."""
+import numpy as np
+import pytest
+import torch
+
+import dsi_synth as S
+from paper_2405_14105_amd import dsi
+from paper_2405_14105_amd.executor import DsiExecutor
+
+from gpu_rig import Rig
+
+pytestmark = pytest.mark.gpu
+
+SEED = 0
+
+
+def greedy_reference(rig, window, w0, N):
+    """The target alone: one greedy token per forward."""
+    out, last = [], int(w0)
+    n = torch.zeros(1, dtype=torch.int32, device=rig.dev)
+    t = torch.zeros(1, dtype=torch.int32, device=rig.dev)
+    for _ in range(N):
+        tk = torch.tensor([[last]], dtype=torch.int32, device=rig.dev)
+        dsi.dsi_verify(rig.model, rig.kv, window, 1, 0, tk, None, None, n, t, 1.0, dsi.DSI_GREEDY, True)
+        last = int(t.item())
+        out.append(last)
+    return out
+
+
+@pytest.mark.parametrize("drafter,T,k,sp", [("same", 0.05, 3, 3), ("tiny_draft", 1.0, 2, 4),
+                                            ("same", 0.05, 1, 8), ("same", 1.0, 4, 2)])
+def test_dsi_returns_the_target_greedy_tokens(drafter, T, k, sp):
+    ts = S.SHAPES["tiny"]
+    L, N, w0 = 30, 24, 11
+    cap = L + N + 8 * (k + 2) + 8
+    dshape, dseed = (ts, SEED) if drafter == "same" else (S.SHAPES[drafter], SEED + S.DRAFT_SEED_OFFSET)
+    prompt = S.prefix_tokens(ts, SEED, 0, L)
+    with Rig(ts, SEED, sp + 1, cap) as trig, Rig(dshape, dseed, 1, cap) as drig:
+        for s in range(sp + 1):
+            trig.prefill(s, prompt)
+        drig.prefill(0, prompt)
+        ex = DsiExecutor(trig.model, trig.kv, drig.model, drig.kv, ts.vocab, k, sp, L,
+                         t_target=1.0, t_drafter=0.1, draft_temperature=T, seed=3)
+        run = ex.generate(w0, N)
+        ref = greedy_reference(trig, sp, w0, N)
+    print(f"{drafter} k={k} sp={sp}: {run.tasks} tasks, {run.rejections} rejections, "
+          f"simulated time {run.time:.2f} (non-SI {N * 1.0:.0f})")
+    assert run.tokens == ref
+    assert run.time <= N * 1.0 + 1e-9

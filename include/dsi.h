@@ -23,7 +23,7 @@
  *  - Work is enqueued on the stream given to dsi_model_create (a hipStream_t,
  *    NULL = the null stream) and is asynchronous unless stated otherwise.
  *  - Data-dependent errors found on the device (a token id outside [0, V),
- *    q(d) not positive and finite) make the affected window output
+ *    q(d) not positive and finite, an invalid token-tree parent) make the affected window output
  *    n = -1, token = -1, leave its KV length unchanged, and make the next
  *    synchronising call (dsi_sync, dsi_kv_length) return DSI_EINVAL.
  *  - A dsi_model's weights are immutable after they are set and the model
@@ -159,6 +159,41 @@ typedef struct {
 
 dsi_status dsi_verify(dsi_model* m, dsi_kv* kv, const dsi_verify_args* args,
                       int32_t* d_n_accepted, int32_t* d_next_token);
+
+/* Token-tree verification with the exact-match rule (Algorithm 1: one
+ * thread per drafter on every prefix, the terminate step, and the j* step
+ * that keeps the smallest-index drafter among those that agree with the
+ * target).  Each of the n_windows windows carries a tree of n_nodes nodes:
+ * node 0 is w0 (the last committed token, not yet cached), node i > 0 is a
+ * draft continuing node parent[i] (0 <= parent[i] < i; children of one node
+ * are numbered in drafter order).  One target forward computes every node's
+ * next-token logits: node i sits at cache slot L_b + i with RoPE position
+ * L_b + depth(i) and attends to the prefix [0, L_b) and to its ancestors'
+ * slots and its own.  The accepted path starts at the root and repeatedly
+ * moves to the smallest-index child whose token equals the target's argmax
+ * (ties to the lowest id) at the current node; n = its number of moves.
+ *   d_tokens [B][n_nodes] int32: node tokens (node 0 = w0)
+ *   d_parent [B][n_nodes] int32: parent[0] = -1, else in [0, i)
+ *   commit: if nonzero, the path's K/V rows are moved to slots L_b+1..L_b+n
+ *           and the window length becomes L_b + n + 1, as if w0 and the
+ *           accepted drafts had been verified as one chain
+ *   d_logits_out (nullable) [B*n_nodes][V] fp32: every node's target logits
+ * Outputs (device): d_path [B][n_nodes] = the accepted nodes (0, a_1..a_n),
+ * -1 beyond; d_n_accepted [B] = n; d_next_token [B] = the target's argmax at
+ * node a_n.  A parent array that breaks the rule above or a token outside
+ * [0, V) gives n = -1, token = -1, path all -1, leaves the length unchanged,
+ * and makes the next synchronising call return DSI_EINVAL.  n_windows *
+ * n_nodes <= DSI_MAX_ROWS; graph replay as for dsi_verify. */
+typedef struct {
+  int32_t window0, n_windows, n_nodes;
+  const int32_t* d_tokens;
+  const int32_t* d_parent;
+  int32_t commit;
+  float* d_logits_out;
+} dsi_tree_args;
+
+dsi_status dsi_verify_tree(dsi_model* m, dsi_kv* kv, const dsi_tree_args* args, int32_t* d_path,
+                           int32_t* d_n_accepted, int32_t* d_next_token);
 
 /* Draft k tokens for one window with a drafter model that shares the
  * target's vocabulary (Section 2: the drafter proposes the lookahead tokens

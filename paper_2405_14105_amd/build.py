@@ -19,7 +19,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 OUT_DIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libdsi.so")
-SOURCES = ["gemm.hip", "attention.hip", "verify.hip", "draft.hip", "elementwise.hip", "runtime.hip"]
+SOURCES = ["gemm.hip", "attention.hip", "verify.hip", "draft.hip", "tree.hip", "elementwise.hip",
+           "runtime.hip"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", shutil.which("hipcc") or "/opt/rocm/bin/hipcc")

@@ -28,7 +28,9 @@ namespace {
 // PIPE: each wave handles several 32-key steps (long prefixes); the loads
 // of its next step are issued as soon as the current step's K (after S) and
 // V (after O) fragments have been consumed, so they overlap the math.
-template <int KVB, int HD, int PIPE>
+// TREE: token-tree rows -- a window key L + j is visible to query row i only
+// if node j is an ancestor of node i (or i itself), per AttnArgs::anc.
+template <int KVB, int HD, int PIPE, int TREE>
 __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
   constexpr int NWV = kAttnWaves;
   constexpr int DS = HD / 32;
@@ -64,6 +66,8 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
   const int qpos = qvalid ? len + ri : -1;
   const int mtok = win * R + ri;
   const int head = kvh * G + gh;
+  unsigned long long anc = ~0ull;
+  if constexpr (TREE) anc = qvalid ? a.anc[mtok] : 0ull;
 
   const size_t kbase = ((size_t)wabs * a.n_kv + kvh) * (size_t)a.maxlen * HD;
   const size_t vbase = ((size_t)wabs * a.n_kv + kvh) * (size_t)HD * a.maxlen;
@@ -176,7 +180,9 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
       for (int j = 0; j < 4; ++j) {
         const int key = p0 + kgrp + t * 4 + j;
         const float v = st[t][j] * a.scale;
-        const float vm = (key <= qpos && key < c1) ? v : -INFINITY;
+        bool vis = key <= qpos && key < c1;
+        if constexpr (TREE) vis = vis && (key < len || ((anc >> ((key - len) & 63)) & 1ull));
+        const float vm = vis ? v : -INFINITY;
         sv[t * 4 + j] = vm;
         mloc = fmaxf(mloc, vm);
       }
@@ -320,10 +326,19 @@ template <int KVB, int HD>
 hipError_t launch_hd(const AttnArgs& a, hipStream_t s) {
   const int units = a.n_chunks * a.n_windows * a.n_kv;
   dim3 g1(((units + 7) / 8) * 8 * a.n_qtiles);
-  if (a.chunk > kAttnChunkQuantum)
-    hipLaunchKernelGGL((k_attn<KVB, HD, 1>), g1, dim3(kAttnWaves * 64), 0, s, a);
-  else
-    hipLaunchKernelGGL((k_attn<KVB, HD, 0>), g1, dim3(kAttnWaves * 64), 0, s, a);
+  const dim3 blk(kAttnWaves * 64);
+  const bool pipe = a.chunk > kAttnChunkQuantum;
+  if (a.anc) {
+    if (pipe)
+      hipLaunchKernelGGL((k_attn<KVB, HD, 1, 1>), g1, blk, 0, s, a);
+    else
+      hipLaunchKernelGGL((k_attn<KVB, HD, 0, 1>), g1, blk, 0, s, a);
+  } else {
+    if (pipe)
+      hipLaunchKernelGGL((k_attn<KVB, HD, 1, 0>), g1, blk, 0, s, a);
+    else
+      hipLaunchKernelGGL((k_attn<KVB, HD, 0, 0>), g1, blk, 0, s, a);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   dim3 g2(HD / 32, a.n_qtiles, a.n_windows * a.n_kv);

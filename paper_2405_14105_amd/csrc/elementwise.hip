@@ -128,7 +128,7 @@ __global__ __launch_bounds__(256) void k_embed_norm(EmbedArgs a) {
   norm_row(v, a.d, m, a.gain, a.eps, a.wtype, a.pack, sh);
   // rotary table of this row's position: angle = pos * base^(-2j/hd), fp64
   const int R = a.rows.rows_per_window;
-  const int pos = a.rows.lens[a.rows.window0 + m / R] + (m % R);
+  const int pos = a.rows.lens[a.rows.window0 + m / R] + (a.rows.depth ? a.rows.depth[m] : m % R);
   const int half = a.hd >> 1;
   for (int j = threadIdx.x; j < half; j += 256) {
     const double inv = exp2(-2.0 * (double)j / (double)a.hd * a.log2_base);

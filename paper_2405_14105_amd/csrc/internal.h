@@ -69,6 +69,10 @@ struct RowMap {         // token row m -> (window, row within window, position)
   const int* lens;      // device window lengths
   int window0;
   int rows_per_window;  // R
+  // nullable: token-tree rows, RoPE position lens[w] + depth[m] (the node's
+  // depth in its tree) instead of lens[w] + (m % R).  The cache slot of row
+  // m is lens[w] + (m % R) either way.
+  const int* depth;
 };
 
 struct EpiArgs {
@@ -160,6 +164,10 @@ struct AttnArgs {
   float2* part_ml;      // [windows*n_kv][qtiles][chunks][16]
   PackRef out;          // O-projection input pack
   int wtype;
+  // nullable: token-tree rows.  Row m may attend to window key L + j
+  // (j < R) only if bit j of anc[m] is set (its ancestors and itself); the
+  // cached prefix [0, L) is visible to every row.
+  const unsigned long long* anc;
 };
 constexpr int kAttnWaves = 8;                       // waves per attention workgroup
 constexpr int kAttnChunkQuantum = kAttnWaves * 32;  // keys per workgroup step
@@ -208,6 +216,36 @@ hipError_t launch_draft_sample(DraftArgs a, void* ws, hipStream_t s);
 size_t verify_workspace_bytes(int rows, int B, int V);
 void verify_bind_workspace(VerifyArgs& a, void* ws, int rows, int B, int V);
 hipError_t launch_verify(const VerifyArgs& a, hipStream_t s);
+// the per-(row, chunk) statistics pass of launch_verify alone (B*(k+1) rows)
+hipError_t launch_verify_rowstats(const VerifyArgs& a, hipStream_t s);
+
+// token trees (tree.hip).  B windows of R nodes; node 0 of each tree is the
+// window's w0, node i > 0 has parent[i] in [0, i).
+struct TreeArgs {
+  int B, R, V, C;
+  const int* tokens;            // [B][R]
+  const int* parent;            // [B][R]
+  int* depth;                   // [B*R]  (prep output)
+  unsigned long long* anc;      // [B*R]  (prep output)
+  int* bad;                     // [B]    (prep output: invalid parent array)
+  const float2* part_arg;       // [B*R][C] chunk (max, argmax) of the logits
+  int* path;                    // [B][R] accepted node path, -1 beyond n
+  int* n_out;
+  int* tok_out;
+  int commit;
+  int* lens;
+  int window0;
+  int* err;
+  int4* decision;               // [B]: (n, L before commit, bad, 0)
+};
+hipError_t launch_tree_prep(const TreeArgs& a, hipStream_t s);
+hipError_t launch_tree_decide(const TreeArgs& a, hipStream_t s);
+// move the K/V rows of each window's accepted path to consecutive slots
+// L+1..L+n (after launch_tree_decide).  kc / vc: cache bases, layer stride
+// layer_elems, window stride win_elems (elements).
+hipError_t launch_tree_compact(const TreeArgs& a, int kv_bf16, void* kc, void* vc, int n_layers,
+                               size_t layer_elems, size_t win_elems, int n_kv, int hd, int maxlen,
+                               hipStream_t s);
 
 // KV and misc (elementwise.hip)
 hipError_t launch_kv_rollback(int* lens, int window, int new_len, int* err, hipStream_t s);

@@ -107,6 +107,11 @@ struct dsi_model {
   float* logits = nullptr;
   void* vws = nullptr;
   void* dws = nullptr;          // drafter-sampling workspace
+  // token trees: per-row depth and ancestor mask, per-window flags/decisions
+  int* tdepth = nullptr;
+  unsigned long long* tanc = nullptr;
+  int* tbad = nullptr;
+  int4* tdec = nullptr;
   int* err = nullptr;
   DevBuf attn_o, attn_ml;
   int live_kv = 0;
@@ -339,13 +344,15 @@ dsi_status plan_attention(dsi_model* m, dsi_kv* kv, int window0, int B, int R, A
   return DSI_OK;
 }
 
-// Stream-ordered launches only (capturable into a graph).
+// Stream-ordered launches only (capturable into a graph).  depth / anc
+// (nullable, device [M]): token-tree rows (RowMap::depth, AttnArgs::anc).
 dsi_status run_forward(dsi_model* m, dsi_kv* kv, const AttnPlan& ap, int window0, int B, int R,
-                       const int* d_tokens, float* logits, int head_last_only, float* hidden) {
+                       const int* d_tokens, float* logits, int head_last_only, float* hidden,
+                       const int* depth = nullptr, const unsigned long long* anc = nullptr) {
   hipStream_t s = m->stream;
   const int M = B * R;
   const int mt = cdiv(M, 16);
-  RowMap rows{kv->lens, window0, R};
+  RowMap rows{kv->lens, window0, R, depth};
   const size_t Md = (size_t)M * m->d;
 
   EmbedArgs ea{};
@@ -393,6 +400,7 @@ dsi_status run_forward(dsi_model* m, dsi_kv* kv, const AttnPlan& ap, int window0
     aa.part_ml = (float2*)m->attn_ml.p;
     aa.out = m->pk_q;
     aa.wtype = m->wtype;
+    aa.anc = anc;
     {
       Prof p(m, DSI_K_ATTN);
       HIP_TRY(launch_attention(m->kvb, m->hd, aa, s));
@@ -466,6 +474,7 @@ dsi_status check_err_word(int* err, hipStream_t s) {
     if (h & 1) what += " token id outside [0, vocab);";
     if (h & 2) what += " verification input invalid (token id or q(d) <= 0);";
     if (h & 4) what += " rollback above the current length;";
+    if (h & 8) what += " token-tree parent array invalid;";
     return fail(DSI_EINVAL, "device-detected input error:%s", what.c_str());
   }
   return DSI_OK;
@@ -606,6 +615,10 @@ dsi_status dsi_model_create(const dsi_config* cfg, void* stream, dsi_model** out
   A((void**)&m->logits, (size_t)kMaxRows * m->V * 4);
   A(&m->vws, verify_workspace_bytes(kMaxRows, kMaxRows, m->V));
   A(&m->dws, draft_workspace_bytes(m->V));
+  A((void**)&m->tdepth, (size_t)kMaxRows * sizeof(int));
+  A((void**)&m->tanc, (size_t)kMaxRows * sizeof(unsigned long long));
+  A((void**)&m->tbad, (size_t)kMaxRows * sizeof(int));
+  A((void**)&m->tdec, (size_t)kMaxRows * sizeof(int4));
 
   A((void**)&m->err, 64);
   if (st != DSI_OK) {
@@ -817,7 +830,7 @@ dsi_status dsi_verify(dsi_model* m, dsi_kv* kv, const dsi_verify_args* a, int32_
     uint32_t tbits;
     memcpy(&tbits, &a->temperature, 4);
     const std::vector<uint64_t> key = {
-        (uint64_t)a->window0, (uint64_t)B, (uint64_t)k, (uint64_t)(uintptr_t)a->d_tokens,
+        1u, (uint64_t)a->window0, (uint64_t)B, (uint64_t)k, (uint64_t)(uintptr_t)a->d_tokens,
         (uint64_t)(uintptr_t)a->d_q, (uint64_t)(uintptr_t)a->d_u, tbits, (uint64_t)a->mode,
         (uint64_t)a->commit, (uint64_t)(uintptr_t)logits, (uint64_t)(uintptr_t)a->d_hidden_out,
         (uint64_t)(uintptr_t)d_n_accepted, (uint64_t)(uintptr_t)d_next_token,
@@ -831,6 +844,88 @@ dsi_status dsi_verify(dsi_model* m, dsi_kv* kv, const dsi_verify_args* a, int32_
   }
   if (a->commit)
     for (int b = 0; b < B; ++b) kv->hi[a->window0 + b] += k + 1;
+  return DSI_OK;
+}
+
+dsi_status dsi_verify_tree(dsi_model* m, dsi_kv* kv, const dsi_tree_args* a, int32_t* d_path,
+                           int32_t* d_n_accepted, int32_t* d_next_token) {
+  if (!m || !kv || !a || kv->m != m) return fail(DSI_EINVAL, "null argument or model / kv mismatch");
+  const int B = a->n_windows, R = a->n_nodes;
+  if (B < 1) return fail(DSI_EINVAL, "n_windows must be >= 1");
+  if (R < 1) return fail(DSI_EINVAL, "n_nodes must be >= 1");
+  if ((long long)B * R > DSI_MAX_ROWS)
+    return fail(DSI_EINVAL, "n_windows*n_nodes = %lld exceeds %d", (long long)B * R, DSI_MAX_ROWS);
+  if (!a->d_tokens || !a->d_parent || !d_path || !d_n_accepted || !d_next_token)
+    return fail(DSI_EINVAL, "null tokens, parents or output pointer");
+  if (a->window0 < 0 || a->window0 + B > kv->n_windows)
+    return fail(DSI_EINVAL, "windows [%d, %d) outside the cache's %d", a->window0, a->window0 + B,
+                kv->n_windows);
+  if (!all_set(m)) return fail(DSI_ESTATE, "not every model tensor has been set");
+  for (int b = 0; b < B; ++b)
+    if (kv->hi[a->window0 + b] + R > kv->max_len)
+      return fail(DSI_ECAPACITY, "window %d: length (<= %lld) + %d exceeds max_len %d", a->window0 + b,
+                  kv->hi[a->window0 + b], R, kv->max_len);
+  float* logits = a->d_logits_out ? a->d_logits_out : m->logits;
+  AttnPlan ap;
+  DSI_TRY(plan_attention(m, kv, a->window0, B, R, &ap));
+  m->last_window0 = a->window0;
+  m->last_B = B;
+  m->last_R = R;
+  // row statistics of the greedy rule over all B*R node rows
+  VerifyArgs va{};
+  va.B = B;
+  va.k = R - 1;
+  va.V = m->V;
+  va.logits = logits;
+  va.temperature = 1.0;
+  va.greedy = 1;
+  verify_bind_workspace(va, m->vws, B * R, B, m->V);
+  TreeArgs ta{};
+  ta.B = B;
+  ta.R = R;
+  ta.V = m->V;
+  ta.C = va.C;
+  ta.tokens = a->d_tokens;
+  ta.parent = a->d_parent;
+  ta.depth = m->tdepth;
+  ta.anc = m->tanc;
+  ta.bad = m->tbad;
+  ta.part_arg = va.part_arg;
+  ta.path = d_path;
+  ta.n_out = d_n_accepted;
+  ta.tok_out = d_next_token;
+  ta.commit = a->commit;
+  ta.lens = kv->lens;
+  ta.window0 = a->window0;
+  ta.err = m->err;
+  ta.decision = m->tdec;
+  const size_t layer_elems = (size_t)kv->n_windows * kv->win_elems;
+  auto launches = [&]() -> dsi_status {
+    HIP_TRY(launch_tree_prep(ta, m->stream));
+    DSI_TRY(run_forward(m, kv, ap, a->window0, B, R, a->d_tokens, logits, 0, nullptr, m->tdepth, m->tanc));
+    Prof p(m, DSI_K_VERIFY);
+    HIP_TRY(launch_verify_rowstats(va, m->stream));
+    HIP_TRY(launch_tree_decide(ta, m->stream));
+    if (a->commit)
+      HIP_TRY(launch_tree_compact(ta, m->kvb, kv->k, kv->v, m->L, layer_elems, kv->win_elems, m->hkv, m->hd,
+                                  kv->maxlen_pad, m->stream));
+    return DSI_OK;
+  };
+  if (m->use_graphs && m->prof_class == 0) {
+    const std::vector<uint64_t> key = {
+        2u, (uint64_t)a->window0, (uint64_t)B, (uint64_t)R, (uint64_t)(uintptr_t)a->d_tokens,
+        (uint64_t)(uintptr_t)a->d_parent, (uint64_t)a->commit, (uint64_t)(uintptr_t)logits,
+        (uint64_t)(uintptr_t)d_path, (uint64_t)(uintptr_t)d_n_accepted, (uint64_t)(uintptr_t)d_next_token,
+        (uint64_t)(uintptr_t)kv->k, (uint64_t)(uintptr_t)kv->v, (uint64_t)(uintptr_t)kv->lens,
+        (uint64_t)kv->n_windows, (uint64_t)kv->max_len, (uint64_t)kv->maxlen_pad,
+        (uint64_t)ap.n_qtiles, (uint64_t)ap.chunk, (uint64_t)ap.n_chunks,
+        (uint64_t)(uintptr_t)m->attn_o.p, (uint64_t)(uintptr_t)m->attn_ml.p};
+    DSI_TRY(replay_or_capture(m, key, launches));
+  } else {
+    DSI_TRY(launches());
+  }
+  if (a->commit)
+    for (int b = 0; b < B; ++b) kv->hi[a->window0 + b] += R;
   return DSI_OK;
 }
 

@@ -370,6 +370,11 @@ void verify_bind_workspace(VerifyArgs& a, void* ws, int rows, int B, int V) {
   a.csum = (double2*)take((size_t)B * C * sizeof(double2));
 }
 
+hipError_t launch_verify_rowstats(const VerifyArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(k_vrow, dim3(a.C, a.B * (a.k + 1)), dim3(VT), 0, s, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_verify(const VerifyArgs& a, hipStream_t s) {
   const int rows = a.B * (a.k + 1);
   hipLaunchKernelGGL(k_vrow, dim3(a.C, rows), dim3(VT), 0, s, a);

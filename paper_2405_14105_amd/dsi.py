@@ -25,8 +25,8 @@ TENSOR_IDS = {
 }
 EXPORTED = (
     "dsi_model_create", "dsi_model_set_tensor", "dsi_model_destroy", "dsi_kv_create",
-    "dsi_kv_destroy", "dsi_prefill", "dsi_verify", "dsi_draft", "dsi_accept", "dsi_kv_rollback",
-    "dsi_kv_length", "dsi_sync", "dsi_kv_export", "dsi_kv_import", "dsi_kv_set_length",
+    "dsi_kv_destroy", "dsi_prefill", "dsi_verify", "dsi_verify_tree", "dsi_draft", "dsi_accept",
+    "dsi_kv_rollback", "dsi_kv_length", "dsi_sync", "dsi_kv_export", "dsi_kv_import", "dsi_kv_set_length",
     "dsi_profile_begin", "dsi_profile_end", "dsi_profile_kernel", "dsi_last_error",
 )
 DSI_K_QKV, DSI_K_ATTN, DSI_K_OPROJ, DSI_K_GATEUP, DSI_K_DOWN, DSI_K_HEAD, DSI_K_VERIFY = range(1, 8)
@@ -56,6 +56,14 @@ class dsi_verify_args(ctypes.Structure):
     ]
 
 
+class dsi_tree_args(ctypes.Structure):
+    _fields_ = [
+        ("window0", ctypes.c_int32), ("n_windows", ctypes.c_int32), ("n_nodes", ctypes.c_int32),
+        ("d_tokens", ctypes.c_void_p), ("d_parent", ctypes.c_void_p), ("commit", ctypes.c_int32),
+        ("d_logits_out", ctypes.c_void_p),
+    ]
+
+
 _lib = None
 
 
@@ -77,6 +85,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "dsi_kv_destroy": ([P], I32),
         "dsi_prefill": ([P, P, I32, P, I32, P], I32),
         "dsi_verify": ([P, P, ctypes.POINTER(dsi_verify_args), P, P], I32),
+        "dsi_verify_tree": ([P, P, ctypes.POINTER(dsi_tree_args), P, P, P], I32),
         "dsi_draft": ([P, P, I32, P, I32, I32, P, F, P, P], I32),
         "dsi_accept": ([P, I32, I32, I32, P, P, P, P, F, I32, P, P], I32),
         "dsi_kv_rollback": ([P, I32, I32], I32),
@@ -152,6 +161,14 @@ def dsi_verify(model: int, kv: int, window0: int, n_windows: int, k: int, d_toke
     a = dsi_verify_args(window0, n_windows, k, _ptr(d_tokens), _ptr(d_q), _ptr(d_u), temperature,
                         mode, int(commit), _ptr(d_logits_out), _ptr(d_hidden_out))
     _check(load().dsi_verify(model, kv, ctypes.byref(a), _ptr(d_n_accepted), _ptr(d_next_token)))
+
+
+def dsi_verify_tree(model: int, kv: int, window0: int, n_windows: int, n_nodes: int, d_tokens, d_parent,
+                    d_path, d_n_accepted, d_next_token, commit: bool = True, d_logits_out=None):
+    a = dsi_tree_args(window0, n_windows, n_nodes, _ptr(d_tokens), _ptr(d_parent), int(commit),
+                      _ptr(d_logits_out))
+    _check(load().dsi_verify_tree(model, kv, ctypes.byref(a), _ptr(d_path), _ptr(d_n_accepted),
+                                  _ptr(d_next_token)))
 
 
 def dsi_draft(model: int, kv: int, window: int, d_feed, n_feed: int, k: int, d_u, d_tokens, d_q,

@@ -81,6 +81,23 @@ class Rig:
             out["hidden"] = hid.cpu().numpy()
         return out
 
+    def verify_tree(self, window0: int, tokens, parent, commit=True, want_logits=True):
+        tokens = np.asarray(tokens, dtype=np.int32)
+        B, R = tokens.shape
+        t = self.dev_i32(tokens)
+        p = self.dev_i32(parent)
+        path = torch.full((B, R), -7, dtype=torch.int32, device=self.dev)
+        n = torch.full((B,), -7, dtype=torch.int32, device=self.dev)
+        tok = torch.full((B,), -7, dtype=torch.int32, device=self.dev)
+        lg = (torch.empty((B * R, self.shape.vocab), dtype=torch.float32, device=self.dev)
+              if want_logits else None)
+        dsi.dsi_verify_tree(self.model, self.kv, window0, B, R, t, p, path, n, tok, commit, lg)
+        torch.cuda.synchronize()
+        out = {"path": path.cpu().numpy(), "n": n.cpu().numpy(), "token": tok.cpu().numpy()}
+        if lg is not None:
+            out["logits"] = lg.cpu().numpy()
+        return out
+
     def length(self, window: int) -> int:
         return dsi.dsi_kv_length(self.kv, window)
 

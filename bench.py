@@ -352,6 +352,91 @@ def run_si(args, wl):
     print(json.dumps(out))
 
 
+def run_tree(args, wl):
+    """Token-tree verification on the workload's target: `--tree-branches`
+    drafters, each proposing a chain of k / branches drafts from the root
+    (the k + 1 rows of the chain step), the last drafter carrying the
+    target's greedy continuation so the commit moves its rows.  Times the
+    tree step (forward, walk, KV compaction; rolled back after each step)
+    beside the greedy chain step over the same number of rows."""
+    import torch
+    from paper_2405_14105_amd import dsi, loader
+
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a GPU (cuda:0)")
+    dsi.load()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_stream(torch.cuda.Stream())
+    stream = torch.cuda.current_stream().cuda_stream
+    shape, k, L = wl.shape, wl.k, wl.prefix_lens[0]
+    nb = args.tree_branches
+    if nb < 1 or k % nb:
+        raise SystemExit(f"--tree-branches must divide k = {k}")
+    D = k // nb
+    model, kv = build_model(dsi, loader, shape, stream, 1, L + k + 1)
+    dsi.dsi_prefill(model, kv, 0, torch.from_numpy(S.prefix_tokens(shape, SEED, 0, L)).to(dev), L, None)
+    V = shape.vocab
+    n_out = torch.zeros(1, dtype=torch.int32, device=dev)
+    t_out = torch.zeros(1, dtype=torch.int32, device=dev)
+    w0, g = 5, []
+    for _ in range(D):
+        t = torch.tensor([[w0] + g], dtype=torch.int32, device=dev)
+        lg = torch.empty((len(g) + 1, V), dtype=torch.float32, device=dev)
+        dsi.dsi_verify(model, kv, 0, 1, len(g), t, None, None, n_out, t_out, 1.0, dsi.DSI_GREEDY,
+                       False, lg)
+        g.append(int(lg[-1].argmax().item()))
+    rng = np.random.default_rng(SEED)
+    toks, par = [w0], [-1]
+    for br in range(nb):
+        chain = g if br == nb - 1 else [int(x) for x in rng.integers(0, V, D)]
+        for j, t in enumerate(chain):
+            par.append(0 if j == 0 else len(toks) - 1)
+            toks.append(t)
+    R = len(toks)
+    dt = torch.tensor([toks], dtype=torch.int32, device=dev)
+    dp = torch.tensor([par], dtype=torch.int32, device=dev)
+    path = torch.zeros((1, R), dtype=torch.int32, device=dev)
+    chain_toks = torch.tensor([[w0] + g + [int(x) for x in rng.integers(0, V, k - D)]],
+                              dtype=torch.int32, device=dev)
+
+    def tree_step():
+        dsi.dsi_verify_tree(model, kv, 0, 1, R, dt, dp, path, n_out, t_out, True)
+        dsi.dsi_kv_rollback(kv, 0, L)
+
+    def chain_step():
+        dsi.dsi_verify(model, kv, 0, 1, k, chain_toks, None, None, n_out, t_out, 1.0,
+                       dsi.DSI_GREEDY, True)
+        dsi.dsi_kv_rollback(kv, 0, L)
+
+    def timed(fn):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / args.steps
+
+    tree_ms = timed(tree_step)
+    n_tree, p = int(n_out.item()), path.cpu().numpy()[0].tolist()
+    chain_ms = timed(chain_step)
+    n_chain = int(n_out.item())
+    dsi.dsi_sync(model)
+    out = {"metric": "token-tree verification step (exact match, one window)",
+           "value": round(1e3 / tree_ms, 2), "unit": "tree steps/s", "steps": args.steps,
+           "warmup": args.warmup, "data": "synthetic",
+           "config": {"workload": shape.name, "prefix": L, "nodes": R, "branches": nb,
+                      "depth": D},
+           "tree_ms": round(tree_ms, 4), "chain_ms": round(chain_ms, 4),
+           "tree_accepted": n_tree, "tree_path": p, "chain_accepted": n_chain}
+    dsi.dsi_kv_destroy(kv)
+    dsi.dsi_model_destroy(model)
+    print(json.dumps(out))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -367,6 +452,9 @@ def main():
                     help="run one 512 MiB device copy first (counter scale reference)")
     ap.add_argument("--si", action="store_true",
                     help="time the draft + verify loop with the workload's drafter instead")
+    ap.add_argument("--tree", action="store_true",
+                    help="time token-tree verification beside the greedy chain step instead")
+    ap.add_argument("--tree-branches", type=int, default=2)
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: this verification step is a single-GPU kernel path "
@@ -376,6 +464,9 @@ def main():
     wl = S.WORKLOADS[args.workload]
     if args.si:
         run_si(args, wl)
+        return
+    if args.tree:
+        run_tree(args, wl)
         return
     g = run_gpu(args, wl)
     sb = step_bytes(wl.shape, wl.prefix_lens, wl.k)

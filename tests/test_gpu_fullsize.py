@@ -24,7 +24,7 @@ import pytest
 import torch
 
 import dsi_synth as S
-from oracle import head64, layer64, softmax64
+from oracle import ancestors, head64, layer64, softmax64, tree_walk
 from paper_2405_14105_amd import dsi
 
 from gpu_rig import Rig
@@ -210,6 +210,59 @@ def test_8b_x7_L1024_k5_batched(rig8b):
         assert rig.length(1 + b) == LENS7[b] + res["n"][b] + 1
         dsi.dsi_kv_rollback(rig.kv, 1 + b, LENS7[b])
         assert rig.length(1 + b) == LENS7[b]
+
+
+def test_8b_L2048_token_tree(rig8b):
+    """Token trees at the 8B shape (two drafters x lookahead 5 = 11 nodes,
+    the rows of the k = 10 chain): a chain tree equals dsi_verify greedy bit
+    for bit; in a branchy tree each node's logits equal a chain verification
+    of its root path (to rounding: the two use different slots and
+    partitions); the walk is the oracle's walk over the GPU's logits; the
+    commit moves exactly the path's K/V rows."""
+    rig, shape = rig8b, rig8b.shape
+    V, L = shape.vocab, L8
+    w0 = 5
+    g = []
+    for _ in range(5):   # the GPU's greedy continuation of prefix + w0
+        o = rig.verify(0, np.array([[w0] + g], np.int32), mode=dsi.DSI_GREEDY, commit=False)
+        g.append(int(np.argmax(o["logits"][-1])))
+    rng = np.random.default_rng(21)
+    rnd = [int(x) for x in rng.integers(0, V, 5)]
+    # chain tree == greedy verification
+    chain = np.array([[w0] + g + rnd], np.int32)
+    a = rig.verify(0, chain, mode=dsi.DSI_GREEDY, commit=False)
+    b = rig.verify_tree(0, chain, np.arange(-1, 10, dtype=np.int32)[None], commit=False)
+    assert np.array_equal(a["logits"], b["logits"])
+    assert (int(b["n"][0]), int(b["token"][0])) == (int(a["n"][0]), int(a["token"][0]))
+    # branchy tree: drafter 1 random (nodes 1..5), drafter 2 the greedy chain (6..10)
+    toks = np.array([w0] + rnd + g, np.int32)
+    par = np.array([-1, 0, 1, 2, 3, 4, 0, 6, 7, 8, 9], np.int32)
+    out = rig.verify_tree(0, toks[None], par[None], commit=False)
+    z = out["logits"]
+    n, tok, path = int(out["n"][0]), int(out["token"][0]), out["path"][0]
+    p_own, t_own, gap = tree_walk(z, toks, par)
+    assert list(path[:n + 1]) == p_own and tok == t_own and (path[n + 1:] == -1).all()
+    say(f"  tree walk: path {p_own}, token {t_own}, min gap {gap:.3g}")
+    for node in (2, 5, 8, 10):
+        root_path = [int(toks[j]) for j in ancestors(par, node)]
+        c = rig.verify(0, np.array([root_path], np.int32), mode=dsi.DSI_GREEDY, commit=False)
+        d = float(np.abs(c["logits"][-1] - z[node]).max())
+        say(f"  node {node}: max|dz| vs chain of its root path = {d:.3g}")
+        assert d <= TOL["bf16"]
+    # commit: rows L + i take the rows of L + path[i]; the prefix is untouched
+    layers = (0, shape.n_layers - 1)
+    pre = {l: rig.export_kv(0, l, L + len(toks)) for l in layers}
+    again = rig.verify_tree(0, toks[None], par[None], commit=True)
+    assert np.array_equal(again["logits"], z) and np.array_equal(again["path"], out["path"])
+    assert rig.length(0) == L + n + 1
+    for l in layers:
+        kg, vg = rig.export_kv(0, l, L + n + 1)
+        for post, before in ((kg, pre[l][0]), (vg, pre[l][1])):
+            assert np.array_equal(post[:L], before[:L])
+            for i in range(n + 1):
+                assert np.array_equal(post[L + i], before[L + path[i]]), (l, i)
+    dsi.dsi_kv_rollback(rig.kv, 0, L)
+    assert rig.length(0) == L
 
 
 # ------------------------------------------------------------ 13B MHA, L 32768, k 10

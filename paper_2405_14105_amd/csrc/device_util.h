@@ -109,6 +109,15 @@ __device__ __forceinline__ void pack_store8(const PackRef& p, int wtype, int m, 
   }
 }
 
+// Device-scope (sc1) 16-byte store: written through to the device's
+// coherence point, for partial results that another workgroup of the same
+// kernel reads with device-scope loads after an arrival counter says they
+// are complete (the writer waits for vmcnt(0) before counting).  One wide
+// store instead of four device-scope dword stores.
+__device__ __forceinline__ void store4_device(float* p, f32x4 v) {
+  asm volatile("global_store_dwordx4 %0, %1, off sc1" ::"v"(p), "v"(v) : "memory");
+}
+
 __device__ __forceinline__ float silu_f(float x) { return x / (1.0f + __expf(-x)); }
 
 }  // namespace dsi

@@ -57,6 +57,20 @@ __device__ __forceinline__ float epilogue(const EpiArgs& e, int nb, int r0, int 
       }
       break;
     }
+    case EPI_PARTRES: {
+      // device-scope stores: written through to the point where the
+      // group's last workgroup reads them (no L2 write-back needed)
+      float* o = e.out + split * e.part_stride + (size_t)m * e.ld;
+      const int n0 = nb * 16 + r0;
+      if (n0 + 3 < e.n_valid) {
+        store4_device(o + n0, s);
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (n0 + j < e.n_valid) __hip_atomic_store(o + n0 + j, s[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+      break;
+    }
     case EPI_PART: {
       float* o = e.out + split * e.part_stride + (size_t)m * e.ld;
 #pragma unroll
@@ -157,6 +171,74 @@ __device__ __forceinline__ void row_scales(const GemmArgs& a, float* rs) {
   }
 }
 
+// EPI_PARTRES tail (see the Epi enum).  The partials are device-scope
+// stores; every wave waits until its stores are complete before the
+// workgroup counts its arrival (a device-scope atomic), and the last arrival
+// reads the partials with device-scope loads, so partials written from
+// another XCD are seen without a write-back or invalidation of any L2.
+// Items are 4 consecutive features of one row, one item per thread (at most
+// MT*16 rows x NBW n-blocks x 4 <= NW*64); the four lanes of one (row,
+// n-block) are adjacent, so the n-block's sum of squares is a two-step
+// butterfly.  The residual and gain values of the thread's item are loaded
+// at the start of the kernel (fold_prefetch), off the critical path.
+struct FoldIn {
+  float4 x, g;
+};
+template <int MT, int NBW, int NW>
+__device__ __forceinline__ FoldIn fold_prefetch(const GemmArgs& a, int nb0, int nbv) {
+  static_assert(MT * NBW <= NW, "one fold item per thread");
+  FoldIn f{};
+  const int it = threadIdx.x;
+  if (it < a.M * nbv * 4) {
+    const int q = it & 3, jm = it >> 2;
+    const int m = jm / nbv, n0 = (nb0 + jm % nbv) * 16 + q * 4;
+    f.x = *(const float4*)(a.epi.x + (size_t)m * a.epi.ld + n0);
+    f.g = *(const float4*)(a.epi.gain + n0);
+  }
+  return f;
+}
+
+template <int WT, int NW>
+__device__ __forceinline__ void part_fold(const GemmArgs& a, int nb0, int nbv, const FoldIn& pre) {
+  __shared__ int s_last;
+  const EpiArgs& e = a.epi;
+  const int g = blockIdx.x / a.S;
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  if (threadIdx.x == 0)
+    s_last = __hip_atomic_fetch_add(e.cnt + g, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == a.S - 1;
+  __syncthreads();
+  if (!s_last) return;
+  {
+    const int it = threadIdx.x;
+    const bool ok = it < a.M * nbv * 4;
+    const int q = it & 3, jm = it >> 2;
+    const int m = ok ? jm / nbv : 0, nb = nb0 + (ok ? jm % nbv : 0);
+    const int n0 = nb * 16 + q * 4;
+    float sq = 0.f;
+    if (ok) {
+      float4 xv = pre.x;
+      for (int sp = 0; sp < a.S; ++sp) {
+        const float* pp = e.out + sp * e.part_stride + (size_t)m * e.ld + n0;
+        xv.x += __hip_atomic_load(pp + 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        xv.y += __hip_atomic_load(pp + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        xv.z += __hip_atomic_load(pp + 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        xv.w += __hip_atomic_load(pp + 3, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+      *(float4*)(e.x + (size_t)m * e.ld + n0) = xv;
+      if (e.copy) *(float4*)(e.copy + (size_t)m * e.ld + n0) = xv;
+      const float4 gv = pre.g;
+      const float y[4] = {xv.x * gv.x, xv.y * gv.y, xv.z * gv.z, xv.w * gv.w};
+      pack_store4(e.pack, WT, m, n0, y);
+      sq = xv.x * xv.x + xv.y * xv.y + xv.z * xv.z + xv.w * xv.w;
+    }
+    sq += __shfl_xor(sq, 1);
+    sq += __shfl_xor(sq, 2);
+    if (ok && q == 0) e.ssq[(size_t)m * a.Nb + nb] = sq;
+  }
+  if (threadIdx.x == 0) __hip_atomic_store(e.cnt + g, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // rs: per-row RMSNorm scales (row_scales) or nullptr.  The iteration count
 // is uniform across a wave, so the EPI_RESID lane reduction is safe.
 // NBW here is the number of n-blocks of one reduction round (red holds
@@ -247,6 +329,8 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(GemmArgs a) {
   if (kb_beg < kb_end) load_w(cur, kb_beg);
   ResidIn pre{};
   if constexpr (EPI == EPI_RESID) pre = resid_prefetch<MT, NBW, NW>(a, nb0);
+  FoldIn fpre{};
+  if constexpr (EPI == EPI_PARTRES) fpre = fold_prefetch<MT, NBW, NW>(a, nb0, nbv);
   if (a.ssq) row_scales<NW>(a, rs);   // overlaps the first weight loads
   for (int kb = kb_beg; kb < kb_end; kb += U) {
     u32x4 nxt[U][NBW];
@@ -288,6 +372,7 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(GemmArgs a) {
     finish<W_BF16, EPI, MT, NBR, NW>(a, red, a.ssq ? rs : nullptr, nb0 + j0, min(NBR, NBW - j0),
                                      wk.split, pre);
   }
+  if constexpr (EPI == EPI_PARTRES) part_fold<W_BF16, NW>(a, nb0, nbv, fpre);
 }
 
 template <int MT, int NBW, int NW, int EPI>
@@ -303,6 +388,8 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_f32(GemmArgs a) {
   const float4* __restrict__ X = (const float4*)a.Xhi;
   ResidIn pre{};
   if constexpr (EPI == EPI_RESID) pre = resid_prefetch<MT, NBW, NW>(a, nb0);
+  FoldIn fpre{};
+  if constexpr (EPI == EPI_PARTRES) fpre = fold_prefetch<MT, NBW, NW>(a, nb0, nbv);
   if (a.ssq) row_scales<NW>(a, rs);
 
   f32x4 acc[NBW][MT];
@@ -342,6 +429,7 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_f32(GemmArgs a) {
     for (int t = 0; t < MT; ++t) red[((w * NBW + j) * MT + t) * 64 + lane] = acc[j][t];
   __syncthreads();
   finish<W_F32, EPI, MT, NBW, NW>(a, red, a.ssq ? rs : nullptr, nb0, NBW, wk.split, pre);
+  if constexpr (EPI == EPI_PARTRES) part_fold<W_F32, NW>(a, nb0, nbv, fpre);
 }
 
 // Grid shaping.  Each wave reuses every activation fragment it loads across
@@ -380,6 +468,8 @@ struct Role<EPI_PART> {
   static constexpr int NW = 16, U = 2;
 };
 template <>
+struct Role<EPI_PARTRES> : Role<EPI_PART> {};
+template <>
 struct Role<EPI_SILU> {
   static constexpr int NW = 12, U = 1;
 };
@@ -411,7 +501,7 @@ hipError_t launch_bf16(const GemmArgs& a, hipStream_t s) {
     else return launch_bf16_cfg<MT, EPI, 2, NW, (U < 2 ? U : 2)>(a, s);
   } else if constexpr (EPI == EPI_QKV) {
     return launch_bf16_cfg<MT, EPI, 2, NW, U>(a, s);
-  } else if constexpr (EPI == EPI_PART) {
+  } else if constexpr (EPI == EPI_PART || EPI == EPI_PARTRES) {
     return launch_bf16_cfg<MT, EPI, 4, NW, 1>(a, s);
   } else if constexpr (EPI == EPI_RESID) {
     return launch_bf16_cfg<MT, EPI, 1, NW, U>(a, s);
@@ -464,13 +554,14 @@ int gemm_part_splits(int wtype, int Nb, int Kb, int mt) {
 
 hipError_t launch_gemm(int wtype, int mt, const GemmArgs& a, hipStream_t s) {
   if (a.Nb <= 0 || a.M <= 0) return hipSuccess;
-  if (a.S < 1 || (a.S > 1 && a.epi.kind != EPI_PART)) return hipErrorInvalidValue;
+  if (a.S < 1 || (a.S > 1 && a.epi.kind != EPI_PART && a.epi.kind != EPI_PARTRES)) return hipErrorInvalidValue;
   switch (a.epi.kind) {
     case EPI_STORE: return launch_epi<EPI_STORE>(wtype, mt, a, s);
     case EPI_PART: return launch_epi<EPI_PART>(wtype, mt, a, s);
     case EPI_QKV: return launch_epi<EPI_QKV>(wtype, mt, a, s);
     case EPI_SILU: return launch_epi<EPI_SILU>(wtype, mt, a, s);
     case EPI_RESID: return launch_epi<EPI_RESID>(wtype, mt, a, s);
+    case EPI_PARTRES: return launch_epi<EPI_PARTRES>(wtype, mt, a, s);
   }
   return hipErrorInvalidValue;
 }

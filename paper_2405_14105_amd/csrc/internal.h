@@ -57,7 +57,12 @@ constexpr int kMaxRows = kMaxMt * 16;
 // 16 features of each n-block in ssq[m * Nb + nb].  The consuming
 // GEMM (GemmArgs::ssq) forms the RMSNorm scale of each row from those sums
 // and applies it to its accumulators: W (x * g) / rms(x) = W RMSNorm(x).
-enum Epi : int { EPI_STORE = 0, EPI_PART = 1, EPI_QKV = 2, EPI_SILU = 3, EPI_RESID = 4 };
+// EPI_PARTRES: EPI_PART, then the last of the S split workgroups of each
+// n-block group to finish (an arrival counter per group, reset by that
+// workgroup) folds x += sum_s partial_s in split order for the group's
+// features and writes what EPI_RESID writes (x, x * gain into the pack,
+// ssq), plus an optional copy of x.
+enum Epi : int { EPI_STORE = 0, EPI_PART = 1, EPI_QKV = 2, EPI_SILU = 3, EPI_RESID = 4, EPI_PARTRES = 5 };
 
 struct PackRef {        // an activation pack (hi/lo bf16, or fp32 in hi)
   void* hi;
@@ -96,6 +101,8 @@ struct EpiArgs {
   float* x;             // [M][ld] residual stream, updated in place
   const float* gain;    // [ld] gain of the RMSNorm that consumes x
   float* ssq;           // [M][Nb] per-n-block sums of x^2
+  int* cnt;             // EPI_PARTRES: [n-block groups] arrival counters (zero between launches)
+  float* copy;          // EPI_PARTRES: nullable [M][ld] copy of the folded x
 };
 
 struct GemmArgs {

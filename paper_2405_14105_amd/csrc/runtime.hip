@@ -101,6 +101,8 @@ struct dsi_model {
   float* x = nullptr;
   float* delta = nullptr;       // [kMaxSplits][kMaxRows][d] K-split partial outputs
   float* ssq = nullptr;         // [kMaxRows][Nb_o] per-n-block sums of x^2 (EPI_RESID)
+  float* ssq2 = nullptr;        // [kMaxRows][Nb_down] the same after the down projection
+  int* gcnt = nullptr;          // EPI_PARTRES arrival counters
   PackRef pk_d{}, pk_q{}, pk_ff{};
   float* qbuf = nullptr;
   float2* rope = nullptr;
@@ -215,7 +217,11 @@ struct Prof {
 //   O       attention pack pk_q -> x += o W_o^T (in place), pk_d = x * g_ffn,
 //           per-n-block sums of x^2 (EPI_RESID)
 //   gate/up pk_d scaled by the RMSNorm of x (ssq) -> SwiGLU pack pk_ff
-//   down    pk_ff -> K-split partials, folded into x by the next RMSNorm
+//   down    pk_ff -> K-split partials; below the last layer the last split
+//           to finish folds them into x and writes the next layer's
+//           attention-norm input pk_d = x * g_attn and ssq2 (EPI_PARTRES);
+//           after the last layer the final RMSNorm folds them
+//   QKV     (layers >= 1) scaled by the RMSNorm of x from ssq2
 //   head    final-normed pack pk_d -> logits
 GemmArgs qkv_args(dsi_model* m, dsi_kv* kv, int l, int M, RowMap rows) {
   GemmArgs g{};
@@ -237,6 +243,12 @@ GemmArgs qkv_args(dsi_model* m, dsi_kv* kv, int l, int M, RowMap rows) {
   g.epi.maxlen = kv->maxlen_pad;
   g.epi.rope = m->rope;
   g.epi.rows = rows;
+  if (l > 0) {   // the previous layer's down projection left x * g_attn and ssq2
+    g.ssq = m->ssq2;
+    g.ssq_n = m->Nb_down;
+    g.norm_d = m->d;
+    g.eps = m->cfg.rms_eps;
+  }
   return g;
 }
 
@@ -278,7 +290,7 @@ GemmArgs gateup_args(dsi_model* m, int l, int M) {
   return g;
 }
 
-GemmArgs down_args(dsi_model* m, int l, int M, int mt) {
+GemmArgs down_args(dsi_model* m, int l, int M, int mt, float* hidden_next = nullptr) {
   GemmArgs g{};
   g.M = M;
   g.W = m->layers[l].wdown;
@@ -292,6 +304,15 @@ GemmArgs down_args(dsi_model* m, int l, int M, int mt) {
   g.epi.ld = m->d;
   g.epi.part_stride = (size_t)kMaxRows * m->d;
   g.epi.n_valid = m->d;
+  if (l + 1 < m->L) {
+    g.epi.kind = EPI_PARTRES;
+    g.epi.x = m->x;
+    g.epi.gain = m->layers[l + 1].attn_norm;
+    g.epi.pack = m->pk_d;
+    g.epi.ssq = m->ssq2;
+    g.epi.cnt = m->gcnt;
+    g.epi.copy = hidden_next;
+  }
   return g;
 }
 
@@ -417,18 +438,14 @@ dsi_status run_forward(dsi_model* m, dsi_kv* kv, const AttnPlan& ap, int window0
       HIP_TRY(launch_gemm(m->wtype, mt, gateup_args(m, l, M), s));
     }
     // down projection into K-split partials
-    const GemmArgs gd = down_args(m, l, M, mt);
+    // down projection; below the last layer it also folds the residual and
+    // prepares the next layer's normed input (EPI_PARTRES)
+    const GemmArgs gd = down_args(m, l, M, mt, hidden ? hidden + (size_t)(l + 1) * Md : nullptr);
     {
       Prof p(m, DSI_K_DOWN);
       HIP_TRY(launch_gemm(m->wtype, mt, gd, s));
     }
     last_splits = gd.S;
-
-    if (l + 1 < m->L) {
-      HIP_TRY(launch_rmsnorm_pack(m->x, m->delta, gd.S, dstride, M, m->d, m->layers[l + 1].attn_norm,
-                                  m->cfg.rms_eps, m->wtype, m->pk_d,
-                                  hidden ? hidden + (size_t)(l + 1) * Md : nullptr, s));
-    }
   }
   if (!logits) {
     // fold the last residual update only when the caller wants hidden states
@@ -607,6 +624,8 @@ dsi_status dsi_model_create(const dsi_config* cfg, void* stream, dsi_model** out
   A((void**)&m->x, (size_t)kMaxRows * m->d * 4);
   A((void**)&m->delta, (size_t)kMaxSplits * kMaxRows * m->d * 4);
   A((void**)&m->ssq, (size_t)m->Nb_o * kMaxRows * 4);
+  A((void**)&m->ssq2, (size_t)m->Nb_down * kMaxRows * 4);
+  A((void**)&m->gcnt, (size_t)(m->Nb_down + 64) * sizeof(int));
   if (st == DSI_OK) m->pk_d = make_pack(m, m->Kb_d, &st);
   if (st == DSI_OK) m->pk_q = make_pack(m, m->Kb_q, &st);
   if (st == DSI_OK) m->pk_ff = make_pack(m, m->Kb_ff, &st);

@@ -1,6 +1,7 @@
 // Causal window-over-prefix attention with grouped KV heads, split over key
 // chunks (one workgroup of eight waves per chunk), plus the log-sum-exp
-// combine of the chunk partials.
+// combine of the chunk partials (a second launch; when the plan has a single
+// chunk the attention kernel normalises its own output instead).
 //
 // Row i of window b (position L_b + i) attends to keys [0, L_b + i]: the
 // cached prefix and the window rows before it (the k+1 prompts of one
@@ -239,6 +240,30 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
 #pragma unroll
   for (int t = 0; t < DT; ++t) so[w][t][lane] = o[t];
   __syncthreads();
+  if (a.n_chunks == 1) {
+    // one key chunk: normalise here, no partials and no combine launch
+    for (int it = threadIdx.x; it < DT * 64; it += NWV * 64) {
+      const int t = it >> 6, l = it & 63, q = l & 15;
+      const int qc = y * 16 + q;
+      if (qc >= G * R) continue;
+      float M = sm[0][q];
+#pragma unroll
+      for (int ww = 1; ww < NWV; ++ww) M = fmaxf(M, sm[ww][q]);
+      const float b = (M == -INFINITY) ? 0.f : M;
+      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+      float L = 0.f;
+#pragma unroll
+      for (int ww = 0; ww < NWV; ++ww) {
+        const float f = expf(sm[ww][q] - b);
+        acc += so[ww][t][l] * f;
+        L += sl[ww][q] * f;
+      }
+      const float inv = 1.0f / L;
+      const float y4[4] = {acc[0] * inv, acc[1] * inv, acc[2] * inv, acc[3] * inv};
+      pack_store4(a.out, a.wtype, win * R + qc % R, (kvh * G + qc / R) * HD + t * 16 + (l >> 4) * 4, y4);
+    }
+    return;
+  }
   const size_t zy = (size_t)z * a.n_qtiles + y;
   const size_t zyc = zy * a.n_chunks + c;
   for (int it = threadIdx.x; it < DT * 64; it += NWV * 64) {
@@ -340,7 +365,7 @@ hipError_t launch_hd(const AttnArgs& a, hipStream_t s) {
       hipLaunchKernelGGL((k_attn<KVB, HD, 0, 0>), g1, blk, 0, s, a);
   }
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || a.n_chunks == 1) return e;
   dim3 g2(HD / 32, a.n_qtiles, a.n_windows * a.n_kv);
   hipLaunchKernelGGL((k_attn_combine<HD>), g2, dim3(128), 0, s, a);
   return hipGetLastError();

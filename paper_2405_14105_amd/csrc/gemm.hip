@@ -500,7 +500,9 @@ hipError_t launch_bf16(const GemmArgs& a, hipStream_t s) {
     else if constexpr (EPI == EPI_STORE) return launch_bf16_cfg<MT, EPI, 8, NW, 1>(a, s);
     else return launch_bf16_cfg<MT, EPI, 2, NW, (U < 2 ? U : 2)>(a, s);
   } else if constexpr (EPI == EPI_QKV) {
-    return launch_bf16_cfg<MT, EPI, 2, NW, U>(a, s);
+    // one n-block per workgroup (e.g. 384 workgroups at the 8B shape): slower
+    // alone than two, faster inside the step (measured over whole steps)
+    return launch_bf16_cfg<MT, EPI, 1, NW, U>(a, s);
   } else if constexpr (EPI == EPI_PART || EPI == EPI_PARTRES) {
     return launch_bf16_cfg<MT, EPI, 4, NW, 1>(a, s);
   } else if constexpr (EPI == EPI_RESID) {

@@ -121,8 +121,11 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
       qf[ds].a = qf[ds].b = float4{0.f, 0.f, 0.f, 0.f};
     }
   }
+  // The first step's loads do not wait for the window length: they are
+  // issued for every step inside the chunk and the allocation (keys beyond
+  // the window are masked, and waves with no step discard them).
   const int pfirst = c0 + 32 * w;
-  if (pfirst < c1) {
+  if (pfirst < min(c0 + a.chunk, a.maxlen)) {
     load_k(pfirst);
     load_v(pfirst);
   }
@@ -294,57 +297,64 @@ __global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
 
 // Log-sum-exp combine of the chunk partials of one (window, KV head, query
 // tile): out = sum_c e^(m_c - M) O_c / sum_c e^(m_c - M) l_c, chunks in
-// order.  grid (HD/32 column slices, query tiles, windows*KV heads); the
-// per-query statistics are formed once in LDS and every thread's chunk loads
-// are independent, so they are in flight together.
+// order.  grid (HD/32 column slices, query tiles, windows*KV heads), one
+// thread per (query, 4 columns).  Each thread loads the (m, l) pairs and
+// partial columns of up to CB chunks at once, so the loads of a batch are in
+// flight together; across batches the running sums are rescaled to the new
+// maximum (with at most CB chunks there is one batch: plain two-pass form).
 template <int HD>
 __global__ __launch_bounds__(128) void k_attn_combine(AttnArgs a) {
-  __shared__ float cb[16], cinv[16];
+  constexpr int CB = 16;
   const int xs = blockIdx.x, y = blockIdx.y, z = blockIdx.z;
   const int win = z / a.n_kv, kvh = z % a.n_kv;
   const int G = a.n_heads / a.n_kv;
   const int R = a.rows.rows_per_window;
   const size_t zy = (size_t)z * a.n_qtiles + y;
-  const float2* ml = a.part_ml + zy * a.n_chunks * 16;
-  if (threadIdx.x < 16) {
-    const int q = threadIdx.x;
-    float M = -INFINITY;
-#pragma unroll 8
-    for (int c = 0; c < a.n_chunks; ++c) M = fmaxf(M, ml[c * 16 + q].x);
-    const float b = (M == -INFINITY) ? 0.f : M;
-    float L = 0.f;
-#pragma unroll 8
-    for (int c = 0; c < a.n_chunks; ++c) {
-      const float2 v = ml[c * 16 + q];
-      L += v.y * expf(v.x - b);
-    }
-    cb[q] = b;
-    cinv[q] = 1.0f / L;
-  }
-  __syncthreads();
   // 128 threads: 16 queries x 8 float4 columns = 32 columns of this slice
   const int q = threadIdx.x >> 3;
   const int d = xs * 32 + (threadIdx.x & 7) * 4;
   const int qi = y * 16 + q;
   if (qi >= G * R) return;
-  const float b = cb[q];
+  const float2* ml = a.part_ml + zy * a.n_chunks * 16 + q;
+  const float* po = a.part_o + (zy * a.n_chunks * 16 + q) * HD + d;
+  float M = -INFINITY, base = 0.f, L = 0.f;
   float4 acc = float4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll 8
-  for (int c = 0; c < a.n_chunks; ++c) {
-    const float f = expf(ml[c * 16 + q].x - b);
-    const float4 v = *(const float4*)(a.part_o + ((zy * a.n_chunks + c) * 16 + q) * HD + d);
-    acc.x += v.x * f;
-    acc.y += v.y * f;
-    acc.z += v.z * f;
-    acc.w += v.w * f;
+  for (int c0 = 0; c0 < a.n_chunks; c0 += CB) {
+    float2 mv[CB];
+    float4 ov[CB];
+#pragma unroll
+    for (int i = 0; i < CB; ++i)
+      if (c0 + i < a.n_chunks) {
+        mv[i] = ml[(size_t)(c0 + i) * 16];
+        ov[i] = *(const float4*)(po + (size_t)(c0 + i) * 16 * HD);
+      }
+#pragma unroll
+    for (int i = 0; i < CB; ++i)
+      if (c0 + i < a.n_chunks) M = fmaxf(M, mv[i].x);
+    const float b = (M == -INFINITY) ? 0.f : M;
+    if (c0 > 0) {
+      const float r = expf(base - b);
+      L *= r;
+      acc.x *= r;
+      acc.y *= r;
+      acc.z *= r;
+      acc.w *= r;
+    }
+    base = b;
+#pragma unroll
+    for (int i = 0; i < CB; ++i)
+      if (c0 + i < a.n_chunks) {
+        const float f = expf(mv[i].x - b);
+        L += mv[i].y * f;
+        acc.x += ov[i].x * f;
+        acc.y += ov[i].y * f;
+        acc.z += ov[i].z * f;
+        acc.w += ov[i].w * f;
+      }
   }
-  const float inv = cinv[q];
-  const int m = win * R + qi % R;
-  const int col = (kvh * G + qi / R) * HD + d;
-  pack_store(a.out, a.wtype, m, col + 0, acc.x * inv);
-  pack_store(a.out, a.wtype, m, col + 1, acc.y * inv);
-  pack_store(a.out, a.wtype, m, col + 2, acc.z * inv);
-  pack_store(a.out, a.wtype, m, col + 3, acc.w * inv);
+  const float inv = 1.0f / L;
+  const float y4[4] = {acc.x * inv, acc.y * inv, acc.z * inv, acc.w * inv};
+  pack_store4(a.out, a.wtype, win * R + qi % R, (kvh * G + qi / R) * HD + d, y4);
 }
 
 template <int KVB, int HD>

@@ -32,8 +32,8 @@ METRIC = "verify-step latency (ms) + verified draft tokens/s, 8B-shape k=10; % H
 # profiles/verify_8b_k10_hbm_traffic.md (FETCH_SIZE x 2.0 + WRITE_SIZE x 1.0,
 # scales from a 512 MiB copy).  Reported only while the GEMM sources are the
 # ones the counters were taken with.
-TRAFFIC_MEASURED = {"workload": "llama8b_L2048_k10", "bytes": 237.83e6,
-                    "sources_sha256": "39401ec5b0de6563fc74160e082646b5cebd18659bb29267707c261d89a90084"}
+TRAFFIC_MEASURED = {"workload": "llama8b_L2048_k10", "bytes": 237.84e6,
+                    "sources_sha256": "2861714118b473cc65aa1c458912ff80b7431eef4532c6195d79e9545998e504"}
 GEMM_SOURCES = ("paper_2405_14105_amd/csrc/gemm.hip", "paper_2405_14105_amd/csrc/device_util.h",
                 "paper_2405_14105_amd/csrc/internal.h")
 HBM_PEAK_GBS = 8000.0

@@ -451,8 +451,9 @@ hipError_t launch_bf16_cfg(GemmArgs a, hipStream_t s) {
 // the wave count and the K-split count -- depends only on the role and the
 // GEMM shape, never on the number of row tiles, so every output element is
 // summed in the same order whether a window is verified alone or in a batch
-// (bit-identical results).  Only the n-blocks per workgroup change with the
-// row-tile count (register budget) and with the output width: the gate/up
+// (bit-identical results).  Only the n-blocks per workgroup and the k-blocks
+// per load batch (neither changes any summation order) change with the
+// row-tile count and with the output width: the gate/up
 // projection takes 7 n-blocks per workgroup when that makes exactly one
 // workgroup per CU (e.g. 1792 n-blocks on 256 CUs); the LM head takes 12
 // (wide output, one k-block per batch).  Measured with 32 layers' weights
@@ -494,10 +495,14 @@ template <int MT, int EPI>
 hipError_t launch_bf16(const GemmArgs& a, hipStream_t s) {
   constexpr int NW = Role<EPI>::NW, U = Role<EPI>::U;
   if constexpr (MT >= 2) {
-    // several row tiles: fewer n-blocks per wave (registers), except the
-    // wide gate/up and LM-head outputs
-    if constexpr (EPI == EPI_SILU) return launch_bf16_cfg<MT, EPI, 4, NW, 1>(a, s);
+    // several row tiles (measured on whole steps of a 42-row batch of 7
+    // windows): one n-block per workgroup for the O projection (256
+    // workgroups), 4 for gate/up with two k-blocks per batch and for the
+    // down projection, 2 for QKV, 8 for the LM head
+    if constexpr (EPI == EPI_SILU) return launch_bf16_cfg<MT, EPI, 4, NW, 2>(a, s);
     else if constexpr (EPI == EPI_STORE) return launch_bf16_cfg<MT, EPI, 8, NW, 1>(a, s);
+    else if constexpr (EPI == EPI_RESID) return launch_bf16_cfg<MT, EPI, 1, NW, U>(a, s);
+    else if constexpr (EPI == EPI_PART || EPI == EPI_PARTRES) return launch_bf16_cfg<MT, EPI, 4, NW, 1>(a, s);
     else return launch_bf16_cfg<MT, EPI, 2, NW, (U < 2 ? U : 2)>(a, s);
   } else if constexpr (EPI == EPI_QKV) {
     // one n-block per workgroup (e.g. 384 workgroups at the 8B shape): slower

@@ -61,6 +61,32 @@ class _Cache:
             self.toks += part
 
 
+def _draft(drafter: int, dcache: _Cache, ctx: list, k: int, V: int, T: float, rng, dev) -> list:
+    """k drafts continuing ctx (whose last token the drafter has not cached):
+    bring the drafter's cache to ctx[:-1] (roll back what diverges, feed what
+    is missing), then dsi_draft."""
+    common = 0
+    for a, b in zip(dcache.toks, ctx[:-1]):
+        if a != b:
+            break
+        common += 1
+    if common < len(dcache.toks):
+        dsi.dsi_kv_rollback(dcache.kv, dcache.window, dcache.base + common)
+        dcache.toks = dcache.toks[:common]
+    feed = ctx[common:]
+    while len(feed) > dsi.DSI_MAX_ROWS:              # catch up long gaps first
+        dcache.sync(dcache.toks + feed[:dsi.DSI_MAX_ROWS], drafter, dev)
+        feed = feed[dsi.DSI_MAX_ROWS:]
+    f = torch.tensor(feed, dtype=torch.int32, device=dev)
+    u = torch.from_numpy(rng.random(k).astype(np.float32)).to(dev)
+    tok = torch.zeros(k + 1, dtype=torch.int32, device=dev)
+    q = torch.empty((k, V), dtype=torch.float32, device=dev)
+    dsi.dsi_draft(drafter, dcache.kv, dcache.window, f, len(feed), k, u, tok, q, T)
+    new = [int(x) for x in tok.cpu().numpy()[1:]]
+    dcache.toks += feed + new[:-1]                   # the feed and d_1..d_{k-1} are cached
+    return new
+
+
 class DsiExecutor:
     """target / drafter: dsi_model handles; tkv: the target's cache with >= sp
     windows, dkv: the drafter's cache (window 0).  All hold the same prompt
@@ -80,29 +106,8 @@ class DsiExecutor:
 
     def _draft_block(self, committed: list, drafts: list) -> None:
         """Extend `drafts` by k drafts continuing committed + drafts."""
-        k, V = self.k, self.V
-        ctx = committed + drafts                       # the last token is not cached yet
-        # the drafter caches ctx[:-1]; feed what it is missing, ending with ctx[-1]
-        common = 0
-        for a, b in zip(self.dcache.toks, ctx[:-1]):
-            if a != b:
-                break
-            common += 1
-        if common < len(self.dcache.toks):
-            dsi.dsi_kv_rollback(self.dcache.kv, 0, self.dcache.base + common)
-            self.dcache.toks = self.dcache.toks[:common]
-        feed = ctx[common:]
-        while len(feed) > dsi.DSI_MAX_ROWS:         # catch up long gaps first
-            self.dcache.sync(self.dcache.toks + feed[:dsi.DSI_MAX_ROWS], self.drafter, self.dev)
-            feed = feed[dsi.DSI_MAX_ROWS:]
-        f = torch.tensor(feed, dtype=torch.int32, device=self.dev)
-        u = torch.from_numpy(self.rng.random(k).astype(np.float32)).to(self.dev)
-        tok = torch.zeros(k + 1, dtype=torch.int32, device=self.dev)
-        q = torch.empty((k, V), dtype=torch.float32, device=self.dev)
-        dsi.dsi_draft(self.drafter, self.dcache.kv, 0, f, len(feed), k, u, tok, q, self.T)
-        new = [int(x) for x in tok.cpu().numpy()[1:]]
-        self.dcache.toks += feed + new[:-1]          # the feed and d_1..d_{k-1} are cached
-        drafts += new
+        drafts += _draft(self.drafter, self.dcache, committed + drafts, self.k, self.V, self.T,
+                         self.rng, self.dev)
 
     def generate(self, w0: int, N: int) -> DsiRun:
         k = self.k
@@ -153,3 +158,63 @@ class DsiExecutor:
                     break
                 j += 1
         return DsiRun(committed[1:N + 1], T0, tasks, rejections)
+
+
+@dataclasses.dataclass
+class TreeRun:
+    tokens: list          # the N generated tokens (after w0)
+    forwards: int         # target forwards (one tree verification each)
+    accepted: list        # drafts accepted by each verification
+
+
+class TreeExecutor:
+    """Algorithm 1's several drafters verified together: every iteration each
+    drafter j = 1..m drafts k tokens continuing the committed tokens (one
+    thread per drafter on the same prefix); the m chains form one token tree
+    rooted at the last committed token (drafter j's chain is numbered after
+    drafter j-1's, so children of a node are in drafter order), and one
+    target forward verifies the whole tree with exact matching and the j*
+    rule (dsi_verify_tree, committed in place).  target / tkv: the target
+    and its cache, verifying in `window`; drafters: (model, kv) pairs, each
+    cache's window 0 holding the prompt.  1 + m k <= DSI_MAX_ROWS."""
+
+    def __init__(self, target: int, tkv: int, window: int, drafters: list, vocab: int, k: int,
+                 prompt_len: int, draft_temperature: float = 1.0, seed: int = 0):
+        if not drafters or 1 + len(drafters) * k > dsi.DSI_MAX_ROWS:
+            raise ValueError("need 1 + drafters * k <= DSI_MAX_ROWS and at least one drafter")
+        self.target, self.tkv, self.window = target, tkv, window
+        self.drafters = [(m, _Cache(kv, 0, prompt_len)) for m, kv in drafters]
+        self.V, self.k, self.T = vocab, k, draft_temperature
+        self.dev = torch.device("cuda:0")
+        self.rng = np.random.default_rng(seed)
+        m = len(drafters)
+        self.R = 1 + m * k
+        par = [-1]
+        for j in range(m):
+            par += [0] + [1 + j * k + i for i in range(k - 1)]
+        self.parent = torch.tensor([par], dtype=torch.int32, device=self.dev)
+        self.path = torch.zeros((1, self.R), dtype=torch.int32, device=self.dev)
+        self.n_out = torch.zeros(1, dtype=torch.int32, device=self.dev)
+        self.t_out = torch.zeros(1, dtype=torch.int32, device=self.dev)
+
+    def generate(self, w0: int, N: int) -> TreeRun:
+        committed = [int(w0)]        # tokens after the prompt; the last one is uncached
+        forwards, accepted = 0, []
+        while len(committed) - 1 < N:
+            nodes = [committed[-1]]
+            for model, cache in self.drafters:
+                nodes += _draft(model, cache, committed, self.k, self.V, self.T, self.rng, self.dev)
+            tk = torch.tensor([nodes], dtype=torch.int32, device=self.dev)
+            dsi.dsi_verify_tree(self.target, self.tkv, self.window, 1, self.R, tk, self.parent, self.path,
+                                self.n_out, self.t_out, True)
+            n, tok = int(self.n_out.item()), int(self.t_out.item())
+            if n < 0:
+                raise RuntimeError("token-tree verification reported an input error")
+            # the host's bound on the window length grows by the node count per
+            # verification; reading the length tightens it to L + n + 1
+            dsi.dsi_kv_length(self.tkv, self.window)
+            path = self.path.cpu().numpy()[0]
+            committed += [nodes[a] for a in path[1:n + 1]] + [tok]
+            forwards += 1
+            accepted.append(n)
+        return TreeRun(committed[1:N + 1], forwards, accepted)

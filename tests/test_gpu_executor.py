@@ -51,3 +51,40 @@ def test_dsi_returns_the_target_greedy_tokens(drafter, T, k, sp):
           f"simulated time {run.time:.2f} (non-SI {N * 1.0:.0f})")
     assert run.tokens == ref
     assert run.time <= N * 1.0 + 1e-9
+
+
+@pytest.mark.parametrize("drafters,k", [(("tiny_draft",), 3), (("tiny_draft", "same"), 3),
+                                        (("same", "tiny_draft", "same"), 2)])
+def test_tree_executor_returns_the_target_greedy_tokens(drafters, k):
+    """Several drafters per iteration, their chains verified as one token tree
+    (exact match + j*): the output is still the target's greedy continuation
+    (Theorem 1), and a drafter equal to the target makes whole chains pass."""
+    from paper_2405_14105_amd.executor import TreeExecutor
+    ts = S.SHAPES["tiny"]
+    L, N, w0 = 30, 24, 11
+    R = 1 + len(drafters) * k
+    prompt = S.prefix_tokens(ts, SEED, 0, L)
+    rigs = []
+    try:
+        trig = Rig(ts, SEED, 2, L + N + R + 8)
+        rigs.append(trig)
+        trig.prefill(0, prompt)
+        trig.prefill(1, prompt)
+        pairs = []
+        for name in drafters:
+            dshape, dseed = (ts, SEED) if name == "same" else (S.SHAPES[name], SEED + S.DRAFT_SEED_OFFSET)
+            drig = Rig(dshape, dseed, 1, L + N + 2 * k + 8)
+            rigs.append(drig)
+            drig.prefill(0, prompt)
+            pairs.append((drig.model, drig.kv))
+        ex = TreeExecutor(trig.model, trig.kv, 0, pairs, ts.vocab, k, L, draft_temperature=0.05, seed=5)
+        run = ex.generate(w0, N)
+        ref = greedy_reference(trig, 1, w0, N)
+    finally:
+        for r in rigs:
+            r.close()
+    print(f"{drafters} k={k}: {run.forwards} target forwards for {N} tokens, accepted {run.accepted}")
+    assert run.tokens == ref
+    assert run.forwards <= N
+    if "same" in drafters:
+        assert run.forwards <= N // 2

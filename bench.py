@@ -211,7 +211,25 @@ def run_gpu(args, wl):
     dsi.dsi_kv_destroy(kv)
     dsi.dsi_model_destroy(model)
     return {"ms": ms, "per_step": per, "kernels": kt, "n_accepted": n_acc.tolist(),
-            "host_us_per_call": enqueue / args.steps * 1e6}
+            "host_us_per_call": enqueue / args.steps * 1e6, "copy_GBs": stream_copy_GBs(torch, dev)}
+
+
+def stream_copy_GBs(torch, dev, nbytes=1 << 30, reps=5):
+    """Measured device-to-device copy bandwidth (bytes read + written per
+    second, best of `reps`): the practical streaming reference."""
+    a = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    b = torch.empty_like(a)
+    a.fill_(1)
+    best = float("inf")
+    for _ in range(reps + 1):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        b.copy_(a)
+        e1.record()
+        torch.cuda.synchronize()
+        best = min(best, e0.elapsed_time(e1))
+    del a, b
+    return 2 * nbytes / (best * 1e-3) / 1e9
 
 
 # ------------------------------------------------------------ CPU baseline
@@ -514,6 +532,8 @@ def main():
         "step_hbm": {"algorithmic_bytes": sb["total"],
                      "achieved_GBs": round(sb["total"] / (ms * 1e-3) / 1e9, 1),
                      "frac_of_peak": round(sb["total"] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
+        "stream_copy": {"GBs": round(g["copy_GBs"], 1), "bytes": 2 << 30,
+                        "step_frac_of_copy": round(sb["total"] / (ms * 1e-3) / 1e9 / g["copy_GBs"], 4)},
         "kernels_ms_per_step": {n: round(v["ms_per_step"], 4) for n, v in g["kernels"].items()},
         "gemm_isolated": {n: {"us": round(v["isolated_avg_ms"] * 1e3, 2),
                               "GBs": round(gb[n] / (v["isolated_avg_ms"] * 1e-3) / 1e9, 1)}

@@ -189,3 +189,24 @@ def test_kv_export_matches_oracle_cache():
                 assert diff.max() <= 2.0 ** -6 * np.abs(o).max()
                 if layer == 0:
                     assert frac < 0.005
+
+
+@pytest.mark.parametrize("name", ["tiny_draft", "ragged_draft"])
+def test_many_key_chunks_end_to_end(name):
+    """A long prefix for a model with few KV heads splits the keys into more
+    than 16 chunks (one KV head group, one query tile: 256-key chunks over
+    ~4.4k keys), so the combine kernel folds the chunk partials in two
+    batches and rescales between them."""
+    shape = S.SHAPES[name]
+    tol = TOL[shape.wdtype]
+    L, k = 4380, 2
+    with Rig(shape, SEED, 1, L + 2 * (k + 1) + 5) as rig:
+        prefix = S.prefix_tokens(shape, SEED, 0, L)
+        rig.prefill(0, prefix)
+        wi = S.window_inputs(shape, SEED, 1, k)
+        out = rig.verify(0, wi["tokens"], mode=dsi.DSI_GREEDY, commit=False)
+    zo = oracle_logits(shape, prefix, wi["tokens"][0])
+    delta = float(np.abs(out["logits"] - zo).max())
+    print(f"{name}: L = {L}, max|dz| = {delta:.3g}")
+    assert delta <= tol
+    split_check(out["logits"], wi["tokens"][0], None, None, out["n"][0], out["token"][0], mode="greedy")

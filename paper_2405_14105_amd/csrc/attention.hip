@@ -31,9 +31,11 @@ namespace {
 // V (after O) fragments have been consumed, so they overlap the math.
 // TREE: token-tree rows -- a window key L + j is visible to query row i only
 // if node j is an ancestor of node i (or i itself), per AttnArgs::anc.
-template <int KVB, int HD, int PIPE, int TREE>
-__global__ __launch_bounds__(kAttnWaves * 64) void k_attn(AttnArgs a) {
-  constexpr int NWV = kAttnWaves;
+// NWV: waves per workgroup, 8, or 4 (many windows in flight: more, smaller
+// workgroups), for bf16 caches with registers capped so that three
+// workgroups share a CU.
+template <int KVB, int HD, int PIPE, int TREE, int NWV>
+__global__ __launch_bounds__(NWV * 64, (NWV == 4 && KVB) ? 3 : 1) void k_attn(AttnArgs a) {
   constexpr int DS = HD / 32;
   constexpr int DT = HD / 16;
   __shared__ float sm[NWV][16];
@@ -357,23 +359,31 @@ __global__ __launch_bounds__(128) void k_attn_combine(AttnArgs a) {
   pack_store4(a.out, a.wtype, win * R + qi % R, (kvh * G + qi / R) * HD + d, y4);
 }
 
+template <int KVB, int HD, int NWV>
+void launch_main(const AttnArgs& a, dim3 grid, hipStream_t s) {
+  const dim3 blk(NWV * 64);
+  const bool pipe = a.chunk > NWV * 32;
+  if (a.anc) {
+    if (pipe)
+      hipLaunchKernelGGL((k_attn<KVB, HD, 1, 1, NWV>), grid, blk, 0, s, a);
+    else
+      hipLaunchKernelGGL((k_attn<KVB, HD, 0, 1, NWV>), grid, blk, 0, s, a);
+  } else {
+    if (pipe)
+      hipLaunchKernelGGL((k_attn<KVB, HD, 1, 0, NWV>), grid, blk, 0, s, a);
+    else
+      hipLaunchKernelGGL((k_attn<KVB, HD, 0, 0, NWV>), grid, blk, 0, s, a);
+  }
+}
+
 template <int KVB, int HD>
 hipError_t launch_hd(const AttnArgs& a, hipStream_t s) {
   const int units = a.n_chunks * a.n_windows * a.n_kv;
   dim3 g1(((units + 7) / 8) * 8 * a.n_qtiles);
-  const dim3 blk(kAttnWaves * 64);
-  const bool pipe = a.chunk > kAttnChunkQuantum;
-  if (a.anc) {
-    if (pipe)
-      hipLaunchKernelGGL((k_attn<KVB, HD, 1, 1>), g1, blk, 0, s, a);
-    else
-      hipLaunchKernelGGL((k_attn<KVB, HD, 0, 1>), g1, blk, 0, s, a);
-  } else {
-    if (pipe)
-      hipLaunchKernelGGL((k_attn<KVB, HD, 1, 0>), g1, blk, 0, s, a);
-    else
-      hipLaunchKernelGGL((k_attn<KVB, HD, 0, 0>), g1, blk, 0, s, a);
-  }
+  if (a.waves == 4)
+    launch_main<KVB, HD, 4>(a, g1, s);
+  else
+    launch_main<KVB, HD, kAttnWaves>(a, g1, s);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.n_chunks == 1) return e;
   dim3 g2(HD / 32, a.n_qtiles, a.n_windows * a.n_kv);
@@ -384,6 +394,8 @@ hipError_t launch_hd(const AttnArgs& a, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_attention(int kv_bf16, int hd, const AttnArgs& a, hipStream_t s) {
+  if (a.waves != 4 && a.waves != kAttnWaves) return hipErrorInvalidValue;
+  if (a.chunk % (a.waves * 32)) return hipErrorInvalidValue;
   if (kv_bf16) {
     switch (hd) {
       case 32: return launch_hd<1, 32>(a, s);

@@ -175,9 +175,9 @@ struct AttnArgs {
   // (j < R) only if bit j of anc[m] is set (its ancestors and itself); the
   // cached prefix [0, L) is visible to every row.
   const unsigned long long* anc;
+  int waves;            // waves per workgroup: kAttnWaves, or 4; chunk % (32 waves) == 0
 };
-constexpr int kAttnWaves = 8;                       // waves per attention workgroup
-constexpr int kAttnChunkQuantum = kAttnWaves * 32;  // keys per workgroup step
+constexpr int kAttnWaves = 8;                       // waves per attention workgroup (default)
 hipError_t launch_attention(int kv_bf16, int hd, const AttnArgs& a, hipStream_t s);
 
 // verification (verify.hip)

@@ -342,7 +342,7 @@ GemmArgs head_args(dsi_model* m, float* logits, int M) {
 // the host bound on lengths; allocates the chunk-partial buffers (so no
 // allocation happens while launches are being captured).
 struct AttnPlan {
-  int n_qtiles = 0, chunk = 0, n_chunks = 0;
+  int n_qtiles = 0, chunk = 0, n_chunks = 0, waves = kAttnWaves;
 };
 
 dsi_status plan_attention(dsi_model* m, dsi_kv* kv, int window0, int B, int R, AttnPlan* p) {
@@ -356,8 +356,19 @@ dsi_status plan_attention(dsi_model* m, dsi_kv* kv, int window0, int B, int R, A
   // about two workgroups per CU for one window (a full second round, not a
   // short tail): at most 512 / (KV heads x query tiles) chunks
   const int want = std::max(1, 512 / (m->hkv * p->n_qtiles));
-  int chunk = (int)round_up((size_t)cdiv(kv->max_len, want), kAttnChunkQuantum);
-  p->chunk = std::min(std::max(chunk, kAttnChunkQuantum), 16384);
+  auto chunk_of = [&](int w, int q) {
+    const int c = (int)round_up((size_t)cdiv(kv->max_len, w), (size_t)q);
+    return std::min(std::max(c, q), 16384);
+  };
+  // A cache with many windows (verification tasks batched together) would
+  // need several rounds of 8-wave workgroups when all its windows are
+  // verified at once: there, 4-wave workgroups with twice the chunks, three
+  // per CU, finish sooner.  The choice depends on the cache's capacity
+  // (windows, max_len), never on the call's batch or lengths.
+  const int q8 = kAttnWaves * 32;
+  const long long full8 = (long long)kv->n_windows * m->hkv * p->n_qtiles * cdiv(kv->max_len, chunk_of(want, q8));
+  p->waves = full8 > 256 ? 4 : kAttnWaves;
+  p->chunk = p->waves == 4 ? chunk_of(2 * want, 4 * 32) : chunk_of(want, q8);
   p->n_chunks = (int)((kmax + p->chunk - 1) / p->chunk);
   const size_t nparts = (size_t)B * m->hkv * p->n_qtiles * p->n_chunks * 16;
   DSI_TRY(ensure(m->attn_o, nparts * m->hd * sizeof(float)));
@@ -422,6 +433,7 @@ dsi_status run_forward(dsi_model* m, dsi_kv* kv, const AttnPlan& ap, int window0
     aa.out = m->pk_q;
     aa.wtype = m->wtype;
     aa.anc = anc;
+    aa.waves = ap.waves;
     {
       Prof p(m, DSI_K_ATTN);
       HIP_TRY(launch_attention(m->kvb, m->hd, aa, s));
@@ -855,7 +867,7 @@ dsi_status dsi_verify(dsi_model* m, dsi_kv* kv, const dsi_verify_args* a, int32_
         (uint64_t)(uintptr_t)d_n_accepted, (uint64_t)(uintptr_t)d_next_token,
         (uint64_t)(uintptr_t)kv->k, (uint64_t)(uintptr_t)kv->v, (uint64_t)(uintptr_t)kv->lens,
         (uint64_t)kv->n_windows, (uint64_t)kv->max_len, (uint64_t)kv->maxlen_pad,
-        (uint64_t)ap.n_qtiles, (uint64_t)ap.chunk, (uint64_t)ap.n_chunks,
+        (uint64_t)ap.n_qtiles, (uint64_t)ap.chunk, (uint64_t)ap.n_chunks, (uint64_t)ap.waves,
         (uint64_t)(uintptr_t)m->attn_o.p, (uint64_t)(uintptr_t)m->attn_ml.p};
     DSI_TRY(replay_or_capture(m, key, launches));
   } else {
@@ -937,7 +949,7 @@ dsi_status dsi_verify_tree(dsi_model* m, dsi_kv* kv, const dsi_tree_args* a, int
         (uint64_t)(uintptr_t)d_path, (uint64_t)(uintptr_t)d_n_accepted, (uint64_t)(uintptr_t)d_next_token,
         (uint64_t)(uintptr_t)kv->k, (uint64_t)(uintptr_t)kv->v, (uint64_t)(uintptr_t)kv->lens,
         (uint64_t)kv->n_windows, (uint64_t)kv->max_len, (uint64_t)kv->maxlen_pad,
-        (uint64_t)ap.n_qtiles, (uint64_t)ap.chunk, (uint64_t)ap.n_chunks,
+        (uint64_t)ap.n_qtiles, (uint64_t)ap.chunk, (uint64_t)ap.n_chunks, (uint64_t)ap.waves,
         (uint64_t)(uintptr_t)m->attn_o.p, (uint64_t)(uintptr_t)m->attn_ml.p};
     DSI_TRY(replay_or_capture(m, key, launches));
   } else {

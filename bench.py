@@ -33,7 +33,7 @@ METRIC = "verify-step latency (ms) + verified draft tokens/s, 8B-shape k=10; % H
 # scales from a 512 MiB copy).  Reported only while the GEMM sources are the
 # ones the counters were taken with.
 TRAFFIC_MEASURED = {"workload": "llama8b_L2048_k10", "bytes": 237.84e6,
-                    "sources_sha256": "2861714118b473cc65aa1c458912ff80b7431eef4532c6195d79e9545998e504"}
+                    "sources_sha256": "d0b88e1e8749886a7f2165b5b656da6ee72aa67301f3c771f3c10f6c19952bb1"}
 GEMM_SOURCES = ("paper_2405_14105_amd/csrc/gemm.hip", "paper_2405_14105_amd/csrc/device_util.h",
                 "paper_2405_14105_amd/csrc/internal.h")
 HBM_PEAK_GBS = 8000.0

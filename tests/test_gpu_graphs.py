@@ -104,3 +104,61 @@ def test_graph_replays_match_eager(name):
         finally:
             eager.close()
             graph.close()
+
+
+def test_tree_graph_replays_match_eager():
+    """dsi_verify_tree through replayed graphs (same buffers, fresh tokens and
+    parent arrays copied in, commits with KV compaction and rollbacks in
+    between) against eager launches, bit-identical including the cache."""
+    shape = S.SHAPES["ragged_bf16"]
+    B, R, lens = 2, 7, [23, 31]
+    rng = np.random.default_rng(4)
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        eager = make_rig(shape, False, B, 120)
+        graph = make_rig(shape, True, B, 120)
+        try:
+            for b in range(B):
+                p = S.prefix_tokens(shape, SEED, b, lens[b])
+                eager.prefill(b, p)
+                graph.prefill(b, p)
+            bufs = []
+            for rig in (eager, graph):
+                d = rig.dev
+                bufs.append({"tok": torch.zeros((B, R), dtype=torch.int32, device=d),
+                             "par": torch.zeros((B, R), dtype=torch.int32, device=d),
+                             "path": torch.zeros((B, R), dtype=torch.int32, device=d),
+                             "n": torch.zeros(B, dtype=torch.int32, device=d),
+                             "t": torch.zeros(B, dtype=torch.int32, device=d),
+                             "z": torch.zeros((B * R, shape.vocab), dtype=torch.float32, device=d)})
+            for it in range(10):
+                toks = rng.integers(0, shape.vocab, (B, R)).astype(np.int32)
+                par = np.full((B, R), -1, np.int32)
+                for b in range(B):
+                    for i in range(1, R):
+                        par[b, i] = rng.integers(0, i)
+                commit = it % 3 != 1
+                outs = []
+                for rig, bf in zip((eager, graph), bufs):
+                    bf["tok"].copy_(torch.from_numpy(toks))
+                    bf["par"].copy_(torch.from_numpy(par))
+                    dsi.dsi_verify_tree(rig.model, rig.kv, 0, B, R, bf["tok"], bf["par"], bf["path"],
+                                        bf["n"], bf["t"], commit, bf["z"])
+                    torch.cuda.synchronize()
+                    outs.append({k: v.cpu().numpy().copy() for k, v in bf.items() if k in ("path", "n", "t", "z")})
+                for key in ("z", "path", "n", "t"):
+                    assert np.array_equal(outs[0][key], outs[1][key]), (it, key)
+                for b in range(B):
+                    Lb = eager.length(b)
+                    assert Lb == graph.length(b), (it, b)
+                    for layer in (0, shape.n_layers - 1):
+                        ke, ve = eager.export_kv(b, layer, Lb)
+                        kg, vg = graph.export_kv(b, layer, Lb)
+                        assert np.array_equal(ke, kg) and np.array_equal(ve, vg), (it, b, layer)
+                if it % 4 == 3:
+                    for b in range(B):
+                        dsi.dsi_kv_rollback(eager.kv, b, lens[b])
+                        dsi.dsi_kv_rollback(graph.kv, b, lens[b])
+        finally:
+            eager.close()
+            graph.close()

@@ -297,6 +297,29 @@ def cpu_baseline(wl, sample_layers: int):
     }
 
 
+def dsi_projection(t_target_ms: float, t_draft_ms: float, sp: int = 7, N: int = 100, runs: int = 50):
+    """Expected generation time of N tokens with the measured latencies fed to
+    the offline simulator (orchestrate.py, the paper's methodology): non-SI,
+    SI at its best lookahead, and DSI with `sp` target servers at the
+    smallest lookahead Equation 1 allows, for a range of acceptance rates
+    (the synthetic drafter and target are unrelated, so the measured rate is
+    not representative)."""
+    from paper_2405_14105_amd import orchestrate as O
+    L = O.lookahead_min(t_target_ms, t_draft_ms, sp)
+    out = {"target_ms": round(t_target_ms, 4), "drafter_ms_per_token": round(t_draft_ms, 4), "sp": sp,
+           "lookahead": L, "tokens": N, "by_acceptance": {}}
+    for a in (0.5, 0.7, 0.9):
+        non = O.simulate_nonsi(t_target_ms, N)
+        si = min(O.expected(O.simulate_si, runs, 0, target_latency=t_target_ms, drafter_latency=t_draft_ms,
+                            lookahead=la, N=N, rate=a) for la in range(1, 21))
+        dsi_t = O.expected(O.simulate_dsi, runs, 0, target_latency=t_target_ms, drafter_latency=t_draft_ms,
+                           lookahead=L, sp=sp, N=N, rate=a)
+        out["by_acceptance"][str(a)] = {"nonsi_ms": round(non, 2), "si_ms": round(si, 2),
+                                        "dsi_ms": round(dsi_t, 2), "dsi_over_si": round(si / dsi_t, 3),
+                                        "dsi_over_nonsi": round(non / dsi_t, 3)}
+    return out
+
+
 def run_si(args, wl):
     """The speculative-inference loop on one GPU: the workload's target and its
     paired drafter (same vocabulary), k drafts per iteration, the drafter rolled
@@ -363,7 +386,8 @@ def run_si(args, wl):
            "draft_ms": round(float(np.mean(draft_ms)), 4),
            "verify_ms": round(float(np.mean(verify_ms)), 4),
            "iteration_ms": round(float(np.mean(iter_ms)), 4),
-           "mean_accepted": round(emitted / iters - 1, 3)}
+           "mean_accepted": round(emitted / iters - 1, 3),
+           "dsi_projection": dsi_projection(float(np.mean(verify_ms)), float(np.mean(draft_ms)) / k)}
     for m, kv in ((target, tkv), (drafter, dkv)):
         dsi.dsi_kv_destroy(kv)
         dsi.dsi_model_destroy(m)

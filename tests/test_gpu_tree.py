@@ -215,3 +215,29 @@ def test_tree_input_errors():
             dsi.dsi_verify_tree(rig.model, rig.kv, 0, 1, 4, t, None, path, n, tok, True)
         assert ei.value.status == dsi.DSI_EINVAL
         assert rig.length(0) == L
+
+
+def test_full_64_node_tree():
+    """The largest tree (64 nodes: all four row tiles, ancestor bit 63), a
+    random shape with long and short branches, against the oracle."""
+    shape = S.SHAPES["tiny"]
+    L, R = 21, 64
+    rng = np.random.default_rng(17)
+    parent = np.array([-1] + [int(rng.integers(max(0, i - 6), i)) for i in range(1, R)], np.int32)
+    parent[63] = 62                                  # a deep chain ending at node 63
+    tokens = rng.integers(0, shape.vocab, R).astype(np.int32)
+    get = getter(shape, SEED)
+    prefix = S.prefix_tokens(shape, SEED, 3, L)
+    _, cache = forward64(shape, get, prefix)
+    zo = tree_logits64(shape, get, cache, tokens, parent)
+    with Rig(shape, SEED, 1, L + R + 4) as rig:
+        rig.prefill(0, prefix)
+        out = rig.verify_tree(0, tokens[None], parent[None], commit=True)
+        z = out["logits"]
+        delta = float(np.abs(z - zo).max())
+        print(f"64-node tree: max|dz| = {delta:.3g}")
+        assert delta <= TOL["f32"]
+        n, tok, path = int(out["n"][0]), int(out["token"][0]), out["path"][0]
+        p_own, t_own, _ = tree_walk(z, tokens, parent)
+        assert list(path[:n + 1]) == p_own and tok == t_own
+        assert rig.length(0) == L + n + 1

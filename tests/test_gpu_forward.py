@@ -210,3 +210,26 @@ def test_many_key_chunks_end_to_end(name):
     print(f"{name}: L = {L}, max|dz| = {delta:.3g}")
     assert delta <= tol
     split_check(out["logits"], wi["tokens"][0], None, None, out["n"][0], out["token"][0], mode="greedy")
+
+
+def test_verify_at_the_row_maximum():
+    """8 windows x (k = 7) + 1 = 64 rows, the most one call carries (four
+    row tiles), ragged prefixes: logits against the oracle per window and
+    each window alone bit-identical."""
+    shape = S.SHAPES["ragged_f32"]
+    B, k = 8, 7
+    lens = [5 + 7 * b for b in range(B)]
+    with Rig(shape, SEED, B, max(lens) + 2 * (k + 1) + 4) as rig:
+        prefixes = [S.prefix_tokens(shape, SEED, b, lens[b]) for b in range(B)]
+        for b in range(B):
+            rig.prefill(b, prefixes[b])
+        wi = S.window_inputs(shape, SEED, B, k)
+        out = rig.verify(0, wi["tokens"], wi["q"], wi["u"], commit=False)
+        z = out["logits"].reshape(B, k + 1, -1)
+        for b in (0, 3, 7):
+            one = rig.verify(b, wi["tokens"][b:b + 1], wi["q"][b:b + 1], wi["u"][b:b + 1], commit=False)
+            assert np.array_equal(one["logits"], z[b])
+    for b in range(B):
+        zo = oracle_logits(shape, prefixes[b], wi["tokens"][b])
+        assert np.abs(z[b] - zo).max() <= TOL["f32"], b
+        split_check(z[b], wi["tokens"][b], wi["q"][b], wi["u"][b], out["n"][b], out["token"][b])

@@ -28,7 +28,9 @@ namespace {
 
 // PIPE: each wave handles several 32-key steps (long prefixes); the loads
 // of its next step are issued as soon as the current step's K (after S) and
-// V (after O) fragments have been consumed, so they overlap the math.
+// V (after O) fragments have been consumed, so they overlap the math.  With
+// PIPE == 2 two register sets alternate and each is refilled with the step
+// two ahead, doubling the bytes in flight per wave.
 // TREE: token-tree rows -- a window key L + j is visible to query row i only
 // if node j is an ancestor of node i (or i itself), per AttnArgs::anc.
 // NWV: waves per workgroup, 8, or 4 (many windows in flight: more, smaller
@@ -77,9 +79,17 @@ __global__ __launch_bounds__(NWV * 64, (NWV == 4 && KVB) ? 3 : 1) void k_attn(At
   const int r16 = lane & 15;
   const int kgrp = (lane >> 4) * 8;
 
-  u32x4 kb16[2][DS], vb16[DT];
-  F8 kf32[2][DS], vf32[DT];
-  auto load_k = [&](int p0) {
+  // K and V of one 32-key step; PIPE == 2 keeps a second set for the step
+  // after the next (bf16 caches only)
+  struct KV16 {
+    u32x4 k[2][DS], v[DT];
+  };
+  struct KV32 {
+    F8 k[2][DS], v[DT];
+  };
+  KV16 b16, b16n;
+  KV32 b32;
+  auto load_k_into = [&](KV16& d16, KV32& d32, int p0) {
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
       const int key = p0 + (r16 >> 2) * 8 + t * 4 + (r16 & 3);
@@ -87,24 +97,24 @@ __global__ __launch_bounds__(NWV * 64, (NWV == 4 && KVB) ? 3 : 1) void k_attn(At
       for (int ds = 0; ds < DS; ++ds) {
         const size_t kidx = kbase + (size_t)key * HD + ds * 32 + kgrp;
         if (KVB) {
-          kb16[t][ds] = *(const u32x4*)((const uint16_t*)a.kc + kidx);
+          d16.k[t][ds] = *(const u32x4*)((const uint16_t*)a.kc + kidx);
         } else {
-          kf32[t][ds].a = *(const float4*)((const float*)a.kc + kidx);
-          kf32[t][ds].b = *(const float4*)((const float*)a.kc + kidx + 4);
+          d32.k[t][ds].a = *(const float4*)((const float*)a.kc + kidx);
+          d32.k[t][ds].b = *(const float4*)((const float*)a.kc + kidx + 4);
         }
       }
     }
   };
-  auto load_v = [&](int p0) {
+  auto load_v_into = [&](KV16& d16, KV32& d32, int p0) {
 #pragma unroll
     for (int t = 0; t < DT; ++t) {
       // 32-key block p0/32 of the blocked V^T cache: dims x 32 keys, contiguous
       const size_t vidx = vbase + ((size_t)(p0 >> 5) * HD + t * 16 + r16) * 32 + kgrp;
       if (KVB) {
-        vb16[t] = *(const u32x4*)((const uint16_t*)a.vc + vidx);
+        d16.v[t] = *(const u32x4*)((const uint16_t*)a.vc + vidx);
       } else {
-        vf32[t].a = *(const float4*)((const float*)a.vc + vidx);
-        vf32[t].b = *(const float4*)((const float*)a.vc + vidx + 4);
+        d32.v[t].a = *(const float4*)((const float*)a.vc + vidx);
+        d32.v[t].b = *(const float4*)((const float*)a.vc + vidx + 4);
       }
     }
   };
@@ -126,10 +136,18 @@ __global__ __launch_bounds__(NWV * 64, (NWV == 4 && KVB) ? 3 : 1) void k_attn(At
   // The first step's loads do not wait for the window length: they are
   // issued for every step inside the chunk and the allocation (keys beyond
   // the window are masked, and waves with no step discard them).
+  const int stride = 32 * NWV;
   const int pfirst = c0 + 32 * w;
-  if (pfirst < min(c0 + a.chunk, a.maxlen)) {
-    load_k(pfirst);
-    load_v(pfirst);
+  const int plim = min(c0 + a.chunk, a.maxlen);
+  if (pfirst < plim) {
+    load_k_into(b16, b32, pfirst);
+    load_v_into(b16, b32, pfirst);
+  }
+  if constexpr (PIPE == 2) {
+    if (pfirst + stride < plim) {
+      load_k_into(b16n, b32, pfirst + stride);
+      load_v_into(b16n, b32, pfirst + stride);
+    }
   }
   bf16x8 qh[DS], ql[DS];
   if (KVB) {
@@ -149,15 +167,10 @@ __global__ __launch_bounds__(NWV * 64, (NWV == 4 && KVB) ? 3 : 1) void k_attn(At
 #pragma unroll
   for (int t = 0; t < DT; ++t) o[t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  for (int p0 = pfirst; p0 < c1; p0 += 32 * NWV) {
-    const int pn = p0 + 32 * NWV;   // this wave's next step
-    if constexpr (!PIPE) {
-      // later steps: every K and V load of the step before any math
-      if (p0 != pfirst) {
-        load_k(p0);
-        load_v(p0);
-      }
-    }
+  // one 32-key step on the K/V held in (d16, d32); with pnext >= 0 the
+  // loads of step pnext go into the same registers as soon as the step's K
+  // (after S) and V (after O) have been consumed
+  auto step = [&](int p0, KV16& d16, KV32& d32, int pnext) {
     f32x4 st[2];
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
@@ -165,18 +178,16 @@ __global__ __launch_bounds__(NWV * 64, (NWV == 4 && KVB) ? 3 : 1) void k_attn(At
 #pragma unroll
       for (int ds = 0; ds < DS; ++ds) {
         if (KVB) {
-          const bf16x8 kb = as_bf16x8(kb16[t][ds]);
+          const bf16x8 kb = as_bf16x8(d16.k[t][ds]);
           st[t] = mfma_bf16(kb, qh[ds], st[t]);
           st[t] = mfma_bf16(kb, ql[ds], st[t]);
         } else {
 #pragma unroll
-          for (int e = 0; e < 8; ++e) st[t] = mfma_f32(f8_get(kf32[t][ds], e), f8_get(qf[ds], e), st[t]);
+          for (int e = 0; e < 8; ++e) st[t] = mfma_f32(f8_get(d32.k[t][ds], e), f8_get(qf[ds], e), st[t]);
         }
       }
     }
-    if constexpr (PIPE) {
-      if (pn < c1) load_k(pn);
-    }
+    if (pnext >= 0 && pnext < c1) load_k_into(d16, d32, pnext);
     // lane holds keys p0 + kgrp + (t*4 + j) for query (lane & 15)
     float sv[8];
     float mloc = -INFINITY;
@@ -220,7 +231,7 @@ __global__ __launch_bounds__(NWV * 64, (NWV == 4 && KVB) ? 3 : 1) void k_attn(At
       }
 #pragma unroll
       for (int t = 0; t < DT; ++t) {
-        const bf16x8 vv = as_bf16x8(vb16[t]);
+        const bf16x8 vv = as_bf16x8(d16.v[t]);
         o[t] = mfma_bf16(vv, ph, o[t]);
         o[t] = mfma_bf16(vv, pl, o[t]);
       }
@@ -228,10 +239,30 @@ __global__ __launch_bounds__(NWV * 64, (NWV == 4 && KVB) ? 3 : 1) void k_attn(At
 #pragma unroll
       for (int t = 0; t < DT; ++t)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) o[t] = mfma_f32(f8_get(vf32[t], e), pv[e], o[t]);
+        for (int e = 0; e < 8; ++e) o[t] = mfma_f32(f8_get(d32.v[t], e), pv[e], o[t]);
     }
-    if constexpr (PIPE) {
-      if (pn < c1) load_v(pn);
+    if (pnext >= 0 && pnext < c1) load_v_into(d16, d32, pnext);
+  };
+
+  if constexpr (PIPE == 2) {
+    // two register sets, each refilled two steps ahead
+    static_assert(KVB, "two-deep pipelining is built for bf16 caches");
+    for (int p0 = pfirst; p0 < c1; p0 += 2 * stride) {
+      step(p0, b16, b32, p0 + 2 * stride);
+      const int p1 = p0 + stride;
+      if (p1 >= c1) break;
+      step(p1, b16n, b32, p1 + 2 * stride);
+    }
+  } else {
+    for (int p0 = pfirst; p0 < c1; p0 += stride) {
+      if constexpr (!PIPE) {
+        // later steps: every K and V load of the step before any math
+        if (p0 != pfirst) {
+          load_k_into(b16, b32, p0);
+          load_v_into(b16, b32, p0);
+        }
+      }
+      step(p0, b16, b32, PIPE ? p0 + stride : -1);
     }
   }
 
@@ -363,6 +394,16 @@ template <int KVB, int HD, int NWV>
 void launch_main(const AttnArgs& a, dim3 grid, hipStream_t s) {
   const dim3 blk(NWV * 64);
   const bool pipe = a.chunk > NWV * 32;
+  if constexpr (KVB && NWV == kAttnWaves) {
+    // three or more steps per wave: refill two steps ahead
+    if (a.chunk >= 3 * NWV * 32) {
+      if (a.anc)
+        hipLaunchKernelGGL((k_attn<KVB, HD, 2, 1, NWV>), grid, blk, 0, s, a);
+      else
+        hipLaunchKernelGGL((k_attn<KVB, HD, 2, 0, NWV>), grid, blk, 0, s, a);
+      return;
+    }
+  }
   if (a.anc) {
     if (pipe)
       hipLaunchKernelGGL((k_attn<KVB, HD, 1, 1, NWV>), grid, blk, 0, s, a);

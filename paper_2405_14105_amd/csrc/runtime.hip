@@ -360,14 +360,17 @@ dsi_status plan_attention(dsi_model* m, dsi_kv* kv, int window0, int B, int R, A
     const int c = (int)round_up((size_t)cdiv(kv->max_len, w), (size_t)q);
     return std::min(std::max(c, q), 16384);
   };
-  // A cache with many windows (verification tasks batched together) would
+  // A cache with many windows (verification tasks batched together) whose
+  // 8-wave plan gives every wave a single 32-key step (latency-bound) would
   // need several rounds of 8-wave workgroups when all its windows are
   // verified at once: there, 4-wave workgroups with twice the chunks, three
-  // per CU, finish sooner.  The choice depends on the cache's capacity
-  // (windows, max_len), never on the call's batch or lengths.
+  // per CU, finish sooner.  Multi-step waves (long prefixes) stay at 8 waves.
+  // The choice depends on the cache's capacity (windows, max_len), never on
+  // the call's batch or lengths.
   const int q8 = kAttnWaves * 32;
-  const long long full8 = (long long)kv->n_windows * m->hkv * p->n_qtiles * cdiv(kv->max_len, chunk_of(want, q8));
-  p->waves = full8 > 256 ? 4 : kAttnWaves;
+  const int chunk8 = chunk_of(want, q8);
+  const long long full8 = (long long)kv->n_windows * m->hkv * p->n_qtiles * cdiv(kv->max_len, chunk8);
+  p->waves = (chunk8 == q8 && full8 > 256) ? 4 : kAttnWaves;
   p->chunk = p->waves == 4 ? chunk_of(2 * want, 4 * 32) : chunk_of(want, q8);
   p->n_chunks = (int)((kmax + p->chunk - 1) / p->chunk);
   const size_t nparts = (size_t)B * m->hkv * p->n_qtiles * p->n_chunks * 16;

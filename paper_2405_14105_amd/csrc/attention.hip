@@ -1,5 +1,5 @@
 // Causal window-over-prefix attention with grouped KV heads, split over key
-// chunks (one workgroup of eight waves per chunk), plus the log-sum-exp
+// chunks (one workgroup of eight, or four, waves per chunk), plus the log-sum-exp
 // combine of the chunk partials (a second launch; when the plan has a single
 // chunk the attention kernel normalises its own output instead).
 //

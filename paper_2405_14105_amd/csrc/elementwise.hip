@@ -21,7 +21,7 @@ __device__ float block_sum_256(float v, float* sh) {
 
 template <typename T>
 __global__ void k_prepack(const T* __restrict__ src, int N, int K, T* __restrict__ dst, int Kb,
-                          int dst_nb0, int n_blocks, int rowmap, int hd, int which) {
+                          int dst_nb0, int n_blocks, int rowmap, int hd, int which, int dst_Nb, int G) {
   const size_t total = (size_t)n_blocks * Kb * 512;
   for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < total;
        i += (size_t)gridDim.x * blockDim.x) {
@@ -46,7 +46,7 @@ __global__ void k_prepack(const T* __restrict__ src, int N, int K, T* __restrict
     }
     if (!mine) continue;
     const T v = (row < N && k < K) ? src[(size_t)row * K + k] : T(0);
-    dst[(((size_t)(dst_nb0 + nbl) * Kb + kb) * 64 + lane) * 8 + e] = v;
+    dst[(wtile_index(dst_nb0 + nbl, kb, dst_Nb, Kb, G) * 64 + lane) * 8 + e] = v;
   }
 }
 
@@ -243,18 +243,19 @@ int grid_for(size_t n, int block) {
 }  // namespace
 
 hipError_t launch_prepack(int wtype, const void* src, int N, int K, void* dst, int Kb, int dst_nb0,
-                          int rowmap, int hd, int which, hipStream_t s) {
+                          int rowmap, int hd, int which, int dst_Nb, int G, hipStream_t s) {
   int n_blocks;
   if (rowmap == 2) n_blocks = (N + 7) / 8;
   else n_blocks = (N + 15) / 16;
+  if (G < 1 || dst_nb0 + n_blocks > dst_Nb) return hipErrorInvalidValue;
   const size_t total = (size_t)n_blocks * Kb * 512;
   const int g = grid_for(total, 256);
   if (wtype == W_BF16)
     hipLaunchKernelGGL(k_prepack<uint16_t>, dim3(g), dim3(256), 0, s, (const uint16_t*)src, N, K,
-                       (uint16_t*)dst, Kb, dst_nb0, n_blocks, rowmap, hd, which);
+                       (uint16_t*)dst, Kb, dst_nb0, n_blocks, rowmap, hd, which, dst_Nb, G);
   else
     hipLaunchKernelGGL(k_prepack<float>, dim3(g), dim3(256), 0, s, (const float*)src, N, K,
-                       (float*)dst, Kb, dst_nb0, n_blocks, rowmap, hd, which);
+                       (float*)dst, Kb, dst_nb0, n_blocks, rowmap, hd, which, dst_Nb, G);
   return hipGetLastError();
 }
 

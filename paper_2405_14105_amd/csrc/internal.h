@@ -111,6 +111,7 @@ struct GemmArgs {
   const void* Xlo;
   int Nb, Kb, M;
   int S;                // K splits across workgroups (EPI_PART only; else 1)
+  int G = 1;            // n-block group of the packed layout (wtile_index)
   EpiArgs epi;
   // optional RMSNorm of the input rows (the pack holds x * gain): the
   // accumulators of row m are scaled by 1/sqrt(sum_nb ssq[m][nb] / norm_d + eps)
@@ -120,16 +121,31 @@ struct GemmArgs {
 };
 // K split the launcher uses for an EPI_PART GEMM of this shape
 int gemm_part_splits(int wtype, int Nb, int Kb, int mt);
+// Packed weight layout.  A matrix of Nb n-blocks x Kb k-blocks is stored as
+// 1 KB tiles (16 rows x 32 k); n-blocks are grouped G at a time and the
+// tiles of a group are k-block major, [group][kb][n-block in group] (the
+// last group may hold fewer than G), so the G tiles of one k-block of a
+// group are contiguous.  G = 1 is the plain [nb][kb] order.
+__host__ __device__ inline size_t wtile_index(int nb, int kb, int Nb, int Kb, int G) {
+  const int g = nb / G, j = nb - g * G;
+  const int gs = Nb - g * G < G ? Nb - g * G : G;
+  return (size_t)g * G * Kb + (size_t)kb * gs + j;
+}
+// Group size the GEMM of this role and shape reads best: the n-blocks per
+// workgroup of its one-row-tile launch (bf16 gate/up and LM head), else 1.
+int gemm_wgroup(int wtype, int epi_kind, int Nb);
 constexpr int kMaxSplits = 4;
 
 // launchers (gemm.hip)
 hipError_t launch_gemm(int wtype, int mt, const GemmArgs& a, hipStream_t s);
 
-// prepack (elementwise.hip): src [N][K] row-major (device), dst packed.
-// rowmap: 0 plain, 1 rope-paired (QKV sections), 2 gate/up interleave
-// (which = 0 gate, 1 up).  dst_nb0: first destination n-block.
+// prepack (elementwise.hip): src [N][K] row-major (device), dst packed
+// (wtile_index with dst_Nb n-blocks in groups of G).  rowmap: 0 plain, 1
+// rope-paired (QKV sections), 2 gate/up interleave (which = 0 gate, 1 up).
+// dst_nb0: first destination n-block.
 hipError_t launch_prepack(int wtype, const void* src, int N, int K, void* dst, int Kb,
-                          int dst_nb0, int rowmap, int hd, int which, hipStream_t s);
+                          int dst_nb0, int rowmap, int hd, int which, int dst_Nb, int G,
+                          hipStream_t s);
 
 // embed gather + RMSNorm + pack + rope table (elementwise.hip)
 struct EmbedArgs {

@@ -91,6 +91,7 @@ struct dsi_model {
   int d = 0, hq = 0, hkv = 0, hd = 0, qdim = 0, kvdim = 0, ff = 0, V = 0, L = 0;
   int Kb_d = 0, Kb_q = 0, Kb_ff = 0;
   int Nb_qkv = 0, Nb_o = 0, Nb_gu = 0, Nb_down = 0, Nb_head = 0;
+  int G_gu = 1, G_head = 1;   // n-block groups of the packed gate/up and LM head
   void* embed = nullptr;
   float* final_norm = nullptr;
   void* lm_head = nullptr;
@@ -280,6 +281,7 @@ GemmArgs gateup_args(dsi_model* m, int l, int M) {
   g.Xlo = m->pk_d.lo;
   g.Nb = m->Nb_gu;
   g.Kb = m->Kb_d;
+  g.G = m->G_gu;
   g.epi.kind = EPI_SILU;
   g.epi.pack = m->pk_ff;
   g.epi.ff = m->ff;
@@ -325,6 +327,7 @@ GemmArgs head_args(dsi_model* m, float* logits, int M) {
   g.Xlo = m->pk_d.lo;
   g.Nb = m->Nb_head;
   g.Kb = m->Kb_d;
+  g.G = m->G_head;
   g.epi.kind = EPI_STORE;
   g.epi.out = logits;
   g.epi.ld = m->V;
@@ -616,6 +619,8 @@ dsi_status dsi_model_create(const dsi_config* cfg, void* stream, dsi_model** out
   m->Nb_gu = cdiv(m->ff, 8);
   m->Nb_down = m->d / 16;
   m->Nb_head = cdiv(m->V, 16);
+  m->G_gu = gemm_wgroup(m->wtype, EPI_SILU, m->Nb_gu);
+  m->G_head = gemm_wgroup(m->wtype, EPI_STORE, m->Nb_head);
   m->layers.resize(m->L);
   m->set_mask.assign(m->L + 1, 0u);
 
@@ -738,14 +743,32 @@ dsi_status dsi_model_set_tensor(dsi_model* m, int32_t layer, int32_t id, const v
     LayerW* lw = global ? nullptr : &m->layers[layer];
     const int nq = m->qdim / 16, nk = m->kvdim / 16;
     switch (id) {
-      case DSI_T_LM_HEAD: e = launch_prepack(m->wtype, dsrc, m->V, m->d, m->lm_head, m->Kb_d, 0, 0, m->hd, 0, nullptr); break;
-      case DSI_T_WQ: e = launch_prepack(m->wtype, dsrc, m->qdim, m->d, lw->wqkv, m->Kb_d, 0, 1, m->hd, 0, nullptr); break;
-      case DSI_T_WK: e = launch_prepack(m->wtype, dsrc, m->kvdim, m->d, lw->wqkv, m->Kb_d, nq, 1, m->hd, 0, nullptr); break;
-      case DSI_T_WV: e = launch_prepack(m->wtype, dsrc, m->kvdim, m->d, lw->wqkv, m->Kb_d, nq + nk, 0, m->hd, 0, nullptr); break;
-      case DSI_T_WO: e = launch_prepack(m->wtype, dsrc, m->d, m->qdim, lw->wo, m->Kb_q, 0, 0, m->hd, 0, nullptr); break;
-      case DSI_T_W_GATE: e = launch_prepack(m->wtype, dsrc, m->ff, m->d, lw->wgu, m->Kb_d, 0, 2, m->hd, 0, nullptr); break;
-      case DSI_T_W_UP: e = launch_prepack(m->wtype, dsrc, m->ff, m->d, lw->wgu, m->Kb_d, 0, 2, m->hd, 1, nullptr); break;
-      case DSI_T_W_DOWN: e = launch_prepack(m->wtype, dsrc, m->d, m->ff, lw->wdown, m->Kb_ff, 0, 0, m->hd, 0, nullptr); break;
+      case DSI_T_LM_HEAD:
+        e = launch_prepack(m->wtype, dsrc, m->V, m->d, m->lm_head, m->Kb_d, 0, 0, m->hd, 0, m->Nb_head, m->G_head,
+                           nullptr);
+        break;
+      case DSI_T_WQ:
+        e = launch_prepack(m->wtype, dsrc, m->qdim, m->d, lw->wqkv, m->Kb_d, 0, 1, m->hd, 0, m->Nb_qkv, 1, nullptr);
+        break;
+      case DSI_T_WK:
+        e = launch_prepack(m->wtype, dsrc, m->kvdim, m->d, lw->wqkv, m->Kb_d, nq, 1, m->hd, 0, m->Nb_qkv, 1, nullptr);
+        break;
+      case DSI_T_WV:
+        e = launch_prepack(m->wtype, dsrc, m->kvdim, m->d, lw->wqkv, m->Kb_d, nq + nk, 0, m->hd, 0, m->Nb_qkv, 1,
+                           nullptr);
+        break;
+      case DSI_T_WO:
+        e = launch_prepack(m->wtype, dsrc, m->d, m->qdim, lw->wo, m->Kb_q, 0, 0, m->hd, 0, m->Nb_o, 1, nullptr);
+        break;
+      case DSI_T_W_GATE:
+        e = launch_prepack(m->wtype, dsrc, m->ff, m->d, lw->wgu, m->Kb_d, 0, 2, m->hd, 0, m->Nb_gu, m->G_gu, nullptr);
+        break;
+      case DSI_T_W_UP:
+        e = launch_prepack(m->wtype, dsrc, m->ff, m->d, lw->wgu, m->Kb_d, 0, 2, m->hd, 1, m->Nb_gu, m->G_gu, nullptr);
+        break;
+      case DSI_T_W_DOWN:
+        e = launch_prepack(m->wtype, dsrc, m->d, m->ff, lw->wdown, m->Kb_ff, 0, 0, m->hd, 0, m->Nb_down, 1, nullptr);
+        break;
     }
     if (e == hipSuccess) e = hipDeviceSynchronize();
     if (staging) hipFree(staging);

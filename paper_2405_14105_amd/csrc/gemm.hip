@@ -28,39 +28,35 @@ namespace {
 // (U), and whether a wave's k-blocks are dealt round-robin (RR: wave w takes
 // k-blocks w, w + NW, ..., so the workgroup's waves read adjacent tiles of
 // the grouped layout at every step) or as one contiguous range.  NW and RR
-// fix the summation order and never change with the row-tile count.  PIPE
-// selects the main loop of one-row-tile launches (see k_gemm_bf16): the
-// two-set weight pipeline, or, for waves of a few k-blocks under a tight
-// register budget, the loop that requests the first two weight batches
-// before any MFMA (which several row tiles always use).
+// fix the summation order and never change with the row-tile count.
 template <int EPI>
 struct Role;
 template <>
 struct Role<EPI_QKV> {
   static constexpr int NW = 16, U = 4;
-  static constexpr bool RR = false, PIPE = false;
+  static constexpr bool RR = false;
 };
 template <>
 struct Role<EPI_PART> {
   static constexpr int NW = 16, U = 2;
-  static constexpr bool RR = false, PIPE = true;
+  static constexpr bool RR = false;
 };
 template <>
 struct Role<EPI_PARTRES> : Role<EPI_PART> {};
 template <>
 struct Role<EPI_SILU> {
   static constexpr int NW = 12, U = 1;
-  static constexpr bool RR = true, PIPE = true;
+  static constexpr bool RR = true;
 };
 template <>
 struct Role<EPI_STORE> {
   static constexpr int NW = 8, U = 1;
-  static constexpr bool RR = true, PIPE = true;
+  static constexpr bool RR = true;
 };
 template <>
 struct Role<EPI_RESID> {
   static constexpr int NW = 16, U = 4;
-  static constexpr bool RR = false, PIPE = true;
+  static constexpr bool RR = false;
 };
 
 // Inputs of the one epilogue item a thread owns, loaded before the main loop
@@ -475,7 +471,7 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(GemmArgs a) {
   const EpiIn pre = epi_prefetch<MT, NBW, NW, EPI>(a, nb0);
   FoldIn fpre{};
   if constexpr (EPI == EPI_PARTRES) fpre = fold_prefetch<MT, NBW, NW>(a, nb0, nbv);
-  if constexpr (Role<EPI>::PIPE && MT == 1) {
+  if constexpr (MT == 1) {
     if (nk > 0) {
       // two weight register sets used in turn (a copy from one to the other
       // would make the compiler wait for a batch before issuing the next)
@@ -514,9 +510,10 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(GemmArgs a) {
       row_scales<NW>(a, spre, rs);
     }
   } else {
-    // Short waves: the first two weight batches are requested before the
-    // first MFMA and the activations are loaded next to their MFMAs (each
-    // of those waits also waits for the weights issued before it).
+    // Several row tiles (MT times the MFMAs and activation fragments per
+    // weight tile, and registers for MT accumulator sets): the first two
+    // weight batches are requested before the first MFMA and the
+    // activations are loaded next to their MFMAs.
     u32x4 cur[U][NBW];
     auto load_w_guarded = [&](u32x4 (&dst)[U][NBW], int i) {
 #pragma unroll
@@ -685,9 +682,12 @@ hipError_t launch_bf16(const GemmArgs& a, hipStream_t s) {
     else if constexpr (EPI == EPI_PART || EPI == EPI_PARTRES) return launch_bf16_cfg<MT, EPI, 4, NW, 1>(a, s);
     else return launch_bf16_cfg<MT, EPI, 2, NW, 2>(a, s);
   } else if constexpr (EPI == EPI_QKV) {
-    // one n-block per workgroup (e.g. 384 workgroups at the 8B shape): slower
-    // alone than two, faster inside the step (measured over whole steps)
-    return launch_bf16_cfg<MT, EPI, 1, NW, U>(a, s);
+    // two n-blocks per workgroup (192 workgroups at the 8B shape, one per CU
+    // with room for both weight register sets): each activation fragment
+    // feeds two weight tiles (measured over whole steps: 8B 3.449 -> 3.425
+    // ms, 13B/32k 10.33 -> 10.25 ms against one n-block on the short-wave
+    // loop)
+    return launch_bf16_cfg<MT, EPI, 2, NW, U>(a, s);
   } else if constexpr (EPI == EPI_PART || EPI == EPI_PARTRES) {
     return launch_bf16_cfg<MT, EPI, 4, NW, 1>(a, s);
   } else if constexpr (EPI == EPI_RESID) {

@@ -32,8 +32,8 @@ METRIC = "verify-step latency (ms) + verified draft tokens/s, 8B-shape k=10; % H
 # profiles/verify_8b_k10_hbm_traffic.md (FETCH_SIZE x 2.0 + WRITE_SIZE x 1.0,
 # scales from a 512 MiB copy).  Reported only while the GEMM sources are the
 # ones the counters were taken with.
-TRAFFIC_MEASURED = {"workload": "llama8b_L2048_k10", "bytes": 237.84e6,
-                    "sources_sha256": "d0b88e1e8749886a7f2165b5b656da6ee72aa67301f3c771f3c10f6c19952bb1"}
+TRAFFIC_MEASURED = {"workload": "llama8b_L2048_k10", "bytes": 237.88e6,
+                    "sources_sha256": "88578a7e39ae7d4dfaa96e80107cfe95d28d2875a630d87e8b1f8114c5b814fa"}
 GEMM_SOURCES = ("paper_2405_14105_amd/csrc/gemm.hip", "paper_2405_14105_amd/csrc/device_util.h",
                 "paper_2405_14105_amd/csrc/internal.h")
 HBM_PEAK_GBS = 8000.0

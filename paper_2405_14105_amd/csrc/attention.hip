@@ -45,7 +45,7 @@ __global__ __launch_bounds__(NWV * 64, (NWV == 4 && KVB) ? 3 : 1) void k_attn(At
   __shared__ f32x4 so[NWV][DT][64];
 
   const int lane = threadIdx.x & 63;
-  const int w = threadIdx.x >> 6;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform: scalar branches
   // XCD-aware order: workgroups are dispatched to the 8 XCDs round-robin by
   // linear id, so ids 8 r + x land on XCD x.  The query tiles of one (chunk,
   // window, KV head) unit u get ids congruent to u mod 8 -- the same XCD and
@@ -125,30 +125,33 @@ __global__ __launch_bounds__(NWV * 64, (NWV == 4 && KVB) ? 3 : 1) void k_attn(At
   F8 qf[DS];
 #pragma unroll
   for (int ds = 0; ds < DS; ++ds) {
+    // unconditional (an invalid lane reads row 0 of its window and zeroes
+    // it), so that later waits count the loads exactly
     const int d0 = ds * 32 + (lane >> 4) * 8;
-    if (qvalid) {
-      qf[ds].a = *(const float4*)(qrow + d0);
-      qf[ds].b = *(const float4*)(qrow + d0 + 4);
-    } else {
-      qf[ds].a = qf[ds].b = float4{0.f, 0.f, 0.f, 0.f};
-    }
+    const float4 qa = *(const float4*)(qrow + d0);
+    const float4 qb = *(const float4*)(qrow + d0 + 4);
+    const float mk = qvalid ? 1.f : 0.f;   // rows are finite: x * 0 = 0
+    qf[ds].a = float4{qa.x * mk, qa.y * mk, qa.z * mk, qa.w * mk};
+    qf[ds].b = float4{qb.x * mk, qb.y * mk, qb.z * mk, qb.w * mk};
   }
   // The first step's loads do not wait for the window length: they are
   // issued for every step inside the chunk and the allocation (keys beyond
-  // the window are masked, and waves with no step discard them).
+  // the window are masked).  A wave whose first step lies past the chunk or
+  // the allocation loads the chunk's last 32 keys instead and discards
+  // them: the loads are unconditional, so the compiler's waits count them
+  // exactly (loads retire in order).  Chunk starts, chunk sizes and the
+  // allocation are multiples of 32, so pfirst < plim implies
+  // pfirst + 32 <= plim.
   const int stride = 32 * NWV;
   const int pfirst = c0 + 32 * w;
   const int plim = min(c0 + a.chunk, a.maxlen);
-  if (pfirst < plim) {
-    load_k_into(b16, b32, pfirst);
-    load_v_into(b16, b32, pfirst);
-  }
+  load_k_into(b16, b32, max(0, min(pfirst, plim - 32)));
+  load_v_into(b16, b32, max(0, min(pfirst, plim - 32)));
   if constexpr (PIPE == 2) {
-    if (pfirst + stride < plim) {
-      load_k_into(b16n, b32, pfirst + stride);
-      load_v_into(b16n, b32, pfirst + stride);
-    }
+    load_k_into(b16n, b32, max(0, min(pfirst + stride, plim - 32)));
+    load_v_into(b16n, b32, max(0, min(pfirst + stride, plim - 32)));
   }
+  __builtin_amdgcn_sched_barrier(0);   // issue them here, not next to their use
   bf16x8 qh[DS], ql[DS];
   if (KVB) {
 #pragma unroll
@@ -253,16 +256,18 @@ __global__ __launch_bounds__(NWV * 64, (NWV == 4 && KVB) ? 3 : 1) void k_attn(At
       if (p1 >= c1) break;
       step(p1, b16n, b32, p1 + 2 * stride);
     }
-  } else {
-    for (int p0 = pfirst; p0 < c1; p0 += stride) {
-      if constexpr (!PIPE) {
-        // later steps: every K and V load of the step before any math
-        if (p0 != pfirst) {
-          load_k_into(b16, b32, p0);
-          load_v_into(b16, b32, p0);
-        }
-      }
-      step(p0, b16, b32, PIPE ? p0 + stride : -1);
+  } else if constexpr (PIPE == 1) {
+    for (int p0 = pfirst; p0 < c1; p0 += stride) step(p0, b16, b32, p0 + stride);
+  } else if (pfirst < c1) {
+    // the first step runs on the loads issued above, outside the loop, so
+    // its S MFMAs wait for its K loads only (loads retire in order, and a
+    // loop header would merge in the later steps' loads); later steps issue
+    // every K and V load of the step before any math
+    step(pfirst, b16, b32, -1);
+    for (int p0 = pfirst + stride; p0 < c1; p0 += stride) {
+      load_k_into(b16, b32, p0);
+      load_v_into(b16, b32, p0);
+      step(p0, b16, b32, -1);
     }
   }
 

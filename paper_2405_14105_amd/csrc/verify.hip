@@ -44,10 +44,15 @@ __global__ __launch_bounds__(VT) void k_vrow(VerifyArgs a) {
   float vals[PER];
   float zmax = -INFINITY;
   int zarg = INT_MAX;
+  // all loads first and unconditional (clamped index, masked after), so
+  // they are in flight together: a wait behind a conditional load is a
+  // wait for every load (loads retire in order)
+#pragma unroll
+  for (int i = 0; i < PER; ++i) vals[i] = z[min(v0 + (int)threadIdx.x + VT * i, v1 - 1)];
 #pragma unroll
   for (int i = 0; i < PER; ++i) {
     const int v = v0 + threadIdx.x + VT * i;
-    vals[i] = v < v1 ? z[v] : -INFINITY;
+    if (v >= v1) vals[i] = -INFINITY;
     if (v < v1 && (vals[i] > zmax || (vals[i] == zmax && v < zarg))) {
       zmax = vals[i];
       zarg = v;
@@ -186,13 +191,31 @@ __global__ __launch_bounds__(VT) void k_vdecide(VerifyArgs a) {
   }
 }
 
-// r_v of entry v for the window's drawing distribution
-__device__ __forceinline__ double draw_mass(const VerifyArgs& a, const float* zrow, const float* qrow,
-                                            double M, double S, bool residual, int v) {
-  const double p = exp((double)zrow[v] / a.temperature - M) / S;
+// r_v of an entry with logit z and drafter probability q for the window's
+// drawing distribution
+__device__ __forceinline__ double entry_mass(const VerifyArgs& a, float z, float q, double M, double S,
+                                             bool residual) {
+  const double p = exp((double)z / a.temperature - M) / S;
   if (!residual) return p;
-  const double d = p - (double)qrow[v];
+  const double d = p - (double)q;
   return d > 0.0 ? d : 0.0;
+}
+
+// The PER logits (and drafter probabilities, when qrow is given) from entry
+// v0 on, all loads issued before any is used (indices clamped into the row,
+// entries past it are never used): a wait behind a conditional load would
+// be a wait for every load (loads retire in order).
+__device__ __forceinline__ void load_entries(const VerifyArgs& a, const float* zrow, const float* qrow, int v0,
+                                             float (&zv)[PER], float (&qv)[PER]) {
+#pragma unroll
+  for (int i = 0; i < PER; ++i) zv[i] = zrow[min(v0 + i, a.V - 1)];
+  if (qrow) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) qv[i] = qrow[min(v0 + i, a.V - 1)];
+  } else {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) qv[i] = 0.f;
+  }
 }
 
 __global__ __launch_bounds__(VT) void k_vresid(VerifyArgs a) {
@@ -206,12 +229,14 @@ __global__ __launch_bounds__(VT) void k_vresid(VerifyArgs a) {
   const float* zrow = a.logits + (size_t)r * a.V;
   const float* qrow = residual ? a.q + ((size_t)b * a.k + n) * a.V : nullptr;
   const int v0 = c * kVerifyChunk + threadIdx.x * PER;
+  float zv[PER], qv[PER];
+  load_entries(a, zrow, qrow, v0, zv, qv);
   double sr = 0.0, sp = 0.0;
+#pragma unroll
   for (int i = 0; i < PER; ++i) {
-    const int v = v0 + i;
-    if (v < a.V) {
-      sr += draw_mass(a, zrow, qrow, st.x, st.y, residual, v);
-      sp += draw_mass(a, zrow, qrow, st.x, st.y, false, v);
+    if (v0 + i < a.V) {
+      sr += entry_mass(a, zv[i], qv[i], st.x, st.y, residual);
+      sp += entry_mass(a, zv[i], qv[i], st.x, st.y, false);
     }
   }
   const double ir = block_scan_incl<VT / 64>(sr, sh);
@@ -300,12 +325,15 @@ __global__ __launch_bounds__(VT) void k_vsample(VerifyArgs a) {
   const float* zrow = a.logits + (size_t)r * a.V;
   const float* qrow = residual ? a.q + ((size_t)b * a.k + n) * a.V : nullptr;
   const int v0 = s_chunk * kVerifyChunk + threadIdx.x * PER;
+  float zv[PER], qv[PER];
+  load_entries(a, zrow, qrow, v0, zv, qv);
   double vals[PER];
   double own = 0.0;
   int lastpos = -1;
+#pragma unroll
   for (int i = 0; i < PER; ++i) {
     const int v = v0 + i;
-    vals[i] = v < a.V ? draw_mass(a, zrow, qrow, st.x, st.y, residual, v) : 0.0;
+    vals[i] = v < a.V ? entry_mass(a, zv[i], qv[i], st.x, st.y, residual) : 0.0;
     own += vals[i];
     if (vals[i] > 0.0) lastpos = v;
   }

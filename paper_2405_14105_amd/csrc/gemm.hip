@@ -307,13 +307,25 @@ __device__ __forceinline__ void part_fold(const GemmArgs& a, int nb0, int nbv, c
     const int n0 = nb * 16 + q * 4;
     float sq = 0.f;
     if (ok) {
+      // every split's values are requested before the first add (split
+      // index clamped; the extra loads are never added), then added in
+      // split order
+      float pv[kMaxSplits][4];
+#pragma unroll
+      for (int sp = 0; sp < kMaxSplits; ++sp) {
+        const float* pp = e.out + min(sp, a.S - 1) * e.part_stride + (size_t)m * e.ld + n0;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) pv[sp][c] = __hip_atomic_load(pp + c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
       float4 xv = pre.x;
-      for (int sp = 0; sp < a.S; ++sp) {
-        const float* pp = e.out + sp * e.part_stride + (size_t)m * e.ld + n0;
-        xv.x += __hip_atomic_load(pp + 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        xv.y += __hip_atomic_load(pp + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        xv.z += __hip_atomic_load(pp + 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        xv.w += __hip_atomic_load(pp + 3, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+      for (int sp = 0; sp < kMaxSplits; ++sp) {
+        if (sp < a.S) {
+          xv.x += pv[sp][0];
+          xv.y += pv[sp][1];
+          xv.z += pv[sp][2];
+          xv.w += pv[sp][3];
+        }
       }
       *(float4*)(e.x + (size_t)m * e.ld + n0) = xv;
       if (e.copy) *(float4*)(e.copy + (size_t)m * e.ld + n0) = xv;

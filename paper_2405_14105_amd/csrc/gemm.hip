@@ -405,6 +405,16 @@ constexpr int red_nb() {
   return NW * NBW * MT <= kRedTiles ? NBW : (kRedTiles / (NW * MT) > 0 ? kRedTiles / (NW * MT) : 1);
 }
 
+// Main loop of a launch: the two-set weight pipeline (one row tile, and up
+// to three row tiles for the QKV, O and gate/up roles, whose shapes leave
+// registers for a second weight set), else the loop that requests the first
+// two weight batches before any MFMA (the down projection and the LM head
+// with several row tiles: their accumulators leave no room; measured on a
+// 42-row batch, pipelining them was slower).
+template <int MT, int EPI>
+constexpr bool kPipelined =
+    MT == 1 || (MT <= 3 && (EPI == EPI_QKV || EPI == EPI_RESID || EPI == EPI_SILU));
+
 template <int MT, int NBW, int NW, int U, int EPI>
 __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(GemmArgs a) {
   constexpr int NBR = red_nb<MT, NBW, NW>();
@@ -483,7 +493,7 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(GemmArgs a) {
   const EpiIn pre = epi_prefetch<MT, NBW, NW, EPI>(a, nb0);
   FoldIn fpre{};
   if constexpr (EPI == EPI_PARTRES) fpre = fold_prefetch<MT, NBW, NW>(a, nb0, nbv);
-  if constexpr (MT == 1) {
+  if constexpr (kPipelined<MT, EPI>) {
     if (nk > 0) {
       // two weight register sets used in turn (a copy from one to the other
       // would make the compiler wait for a batch before issuing the next)
@@ -522,10 +532,9 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(GemmArgs a) {
       row_scales<NW>(a, spre, rs);
     }
   } else {
-    // Several row tiles (MT times the MFMAs and activation fragments per
-    // weight tile, and registers for MT accumulator sets): the first two
-    // weight batches are requested before the first MFMA and the
-    // activations are loaded next to their MFMAs.
+    // The first two weight batches are requested before the first MFMA and
+    // the activations are loaded next to their MFMAs (each of those waits
+    // also waits for the weights issued before it).
     u32x4 cur[U][NBW];
     auto load_w_guarded = [&](u32x4 (&dst)[U][NBW], int i) {
 #pragma unroll
@@ -684,15 +693,16 @@ hipError_t launch_bf16(const GemmArgs& a, hipStream_t s) {
   if constexpr (MT >= 2) {
     // several row tiles (measured on whole steps of a 42-row batch of 7
     // windows): one n-block per workgroup for the O projection (256
-    // workgroups), 4 for gate/up with two k-blocks per batch and for the
-    // down projection, 2 for QKV, 8 for the LM head
-    // (all with the short-wave loop: several row tiles already give each
-    // wave MT times the MFMAs per weight tile)
-    if constexpr (EPI == EPI_SILU) return launch_bf16_cfg<MT, EPI, 4, NW, 2>(a, s);
+    // workgroups), 4 for gate/up and for the down projection, 2 for QKV, 8
+    // for the LM head; the k-blocks per batch of the pipelined roles keep
+    // both weight register sets and a batch of activations within the
+    // register budget (three row tiles: gate/up and QKV one, O two)
+    constexpr bool P = kPipelined<MT, EPI>;
+    if constexpr (EPI == EPI_SILU) return launch_bf16_cfg<MT, EPI, 4, NW, (P ? 1 : 2)>(a, s);
     else if constexpr (EPI == EPI_STORE) return launch_bf16_cfg<MT, EPI, 8, NW, 1>(a, s);
-    else if constexpr (EPI == EPI_RESID) return launch_bf16_cfg<MT, EPI, 1, NW, U>(a, s);
+    else if constexpr (EPI == EPI_RESID) return launch_bf16_cfg<MT, EPI, 1, NW, (P ? 2 : U)>(a, s);
     else if constexpr (EPI == EPI_PART || EPI == EPI_PARTRES) return launch_bf16_cfg<MT, EPI, 4, NW, 1>(a, s);
-    else return launch_bf16_cfg<MT, EPI, 2, NW, 2>(a, s);
+    else return launch_bf16_cfg<MT, EPI, 2, NW, (MT == 3 ? 1 : 2)>(a, s);
   } else if constexpr (EPI == EPI_QKV) {
     // two n-blocks per workgroup (192 workgroups at the 8B shape, one per CU
     // with room for both weight register sets): each activation fragment

@@ -33,7 +33,7 @@ METRIC = "verify-step latency (ms) + verified draft tokens/s, 8B-shape k=10; % H
 # scales from a 512 MiB copy).  Reported only while the GEMM sources are the
 # ones the counters were taken with.
 TRAFFIC_MEASURED = {"workload": "llama8b_L2048_k10", "bytes": 237.88e6,
-                    "sources_sha256": "88578a7e39ae7d4dfaa96e80107cfe95d28d2875a630d87e8b1f8114c5b814fa"}
+                    "sources_sha256": "36198cd8487d4aab03429d3b473518ab695c196b7ea43829a288348a5f1037db"}
 GEMM_SOURCES = ("paper_2405_14105_amd/csrc/gemm.hip", "paper_2405_14105_amd/csrc/device_util.h",
                 "paper_2405_14105_amd/csrc/internal.h")
 HBM_PEAK_GBS = 8000.0

@@ -36,9 +36,10 @@ __global__ __launch_bounds__(ST) void k_dstat(DraftArgs a) {
   float vals[SPER];
   float zmax = -INFINITY;
 #pragma unroll
+  for (int i = 0; i < SPER; ++i) vals[i] = a.logits[min(v0 + (int)threadIdx.x + ST * i, v1 - 1)];
+#pragma unroll
   for (int i = 0; i < SPER; ++i) {
-    const int v = v0 + threadIdx.x + ST * i;
-    vals[i] = v < v1 ? a.logits[v] : -INFINITY;
+    if (v0 + (int)threadIdx.x + ST * i >= v1) vals[i] = -INFINITY;
     zmax = fmaxf(zmax, vals[i]);
   }
 #pragma unroll
@@ -91,11 +92,14 @@ __global__ __launch_bounds__(ST) void k_dq(DraftArgs a) {
   // thread t: entries c*4096 + 16 t .. +15 in order (the rescan's order)
   const int v0 = c * kVerifyChunk + threadIdx.x * SPER;
   double own = 0.0;
+  float zv[SPER];
+#pragma unroll
+  for (int i = 0; i < SPER; ++i) zv[i] = a.logits[min(v0 + i, a.V - 1)];
 #pragma unroll
   for (int i = 0; i < SPER; ++i) {
     const int v = v0 + i;
     if (v < a.V) {
-      const float q = (float)(exp((double)a.logits[v] / a.temperature - M) / S);
+      const float q = (float)(exp((double)zv[i] / a.temperature - M) / S);
       a.q_out[v] = q;
       own += (double)q;
     }
@@ -166,10 +170,15 @@ __global__ __launch_bounds__(ST) void k_ddraw(DraftArgs a) {
   double vals[SPER];
   double own = 0.0;
   int lastpos = -1;
+  // all loads first (clamped index, masked after): a wait behind a
+  // conditional load is a wait for every load issued before it
+  float qv[SPER];
+#pragma unroll
+  for (int i = 0; i < SPER; ++i) qv[i] = a.q_out[min(v0 + i, a.V - 1)];
 #pragma unroll
   for (int i = 0; i < SPER; ++i) {
     const int v = v0 + i;
-    vals[i] = v < a.V ? (double)a.q_out[v] : 0.0;
+    vals[i] = v < a.V ? (double)qv[i] : 0.0;
     own += vals[i];
     if (vals[i] > 0.0) lastpos = v;
   }

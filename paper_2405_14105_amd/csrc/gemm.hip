@@ -709,8 +709,11 @@ hipError_t launch_bf16(const GemmArgs& a, hipStream_t s) {
     // feeds two weight tiles (measured over whole steps: 8B 3.449 -> 3.425
     // ms, 13B/32k 10.33 -> 10.25 ms against one n-block on the short-wave
     // loop); four (two k-blocks per batch for the registers) when two would
-    // still need a second round of workgroups (13B/32k 10.08 -> 9.81 ms)
+    // still need a second round of workgroups (13B/32k 10.08 -> 9.81 ms), one
+    // when one round of single-n-block workgroups covers them all (1B
+    // 0.886 -> 0.868 ms)
     if (a.Nb > 512) return launch_bf16_cfg<MT, EPI, 4, NW, 2>(a, s);
+    if (a.Nb <= 256) return launch_bf16_cfg<MT, EPI, 1, NW, U>(a, s);
     return launch_bf16_cfg<MT, EPI, 2, NW, U>(a, s);
   } else if constexpr (EPI == EPI_PART || EPI == EPI_PARTRES) {
     return launch_bf16_cfg<MT, EPI, 4, NW, 1>(a, s);

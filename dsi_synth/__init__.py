@@ -92,6 +92,13 @@ SHAPES = {
                         kvdtype="f32", gains="random"),
     "gqa_hd64": Shape("gqa_hd64", 3, 256, 8, 2, 64, 688, 2050, gains="random"),
     "mha_hd128": Shape("mha_hd128", 2, 256, 2, 2, 128, 520, 1536, gains="random"),
+    # mixed storage types and head_dim 96: bf16 weights over an fp32 cache,
+    # fp32 weights over a bf16 cache
+    "hd96_kvf32": Shape("hd96_kvf32", 2, 224, 3, 1, 96, 376, 1111, kvdtype="f32", gains="random"),
+    "f32w_bf16kv": Shape("f32w_bf16kv", 2, 160, 4, 2, 64, 300, 901, wdtype="f32", gains="random"),
+    # many KV heads and query tiles: few key chunks per (window, KV head),
+    # so waves take several 32-key steps once the cache is a few thousand long
+    "many_kv": Shape("many_kv", 2, 256, 64, 16, 32, 400, 1500, gains="random"),
     # drafters: small models sharing a target's vocabulary
     "tiny_draft": Shape("tiny_draft", 1, 64, 2, 2, 32, 128, 1024, wdtype="f32", kvdtype="f32"),
     "ragged_draft": Shape("ragged_draft", 1, 96, 3, 1, 32, 200, 1003, gains="random"),

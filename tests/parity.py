@@ -23,6 +23,13 @@ from oracle import forward64, verify64
 TOL = {"f32": 1e-4, "bf16": 2e-2}
 
 
+def tol_of(shape) -> float:
+    """Logit tolerance of a shape: the bf16 one as soon as weights or the KV
+    cache are stored in bf16 (rounding of a cached K/V element near a
+    rounding boundary may go either way on the two sides)."""
+    return TOL["bf16"] if "bf16" in (shape.wdtype, shape.kvdtype) else TOL["f32"]
+
+
 def getter(shape, seed=0, cache=True):
     """get(layer, name) -> fp64 weights for the oracle (memoised if cache)."""
     memo = {}

@@ -19,7 +19,7 @@ from oracle import forward64
 from paper_2405_14105_amd import dsi
 
 from gpu_rig import Rig
-from parity import TOL, e2e_check, getter, oracle_logits, split_check
+from parity import TOL, e2e_check, getter, oracle_logits, split_check, tol_of
 
 pytestmark = pytest.mark.gpu
 
@@ -32,13 +32,15 @@ CASES = [
     ("ragged_bf16", 45, 6),
     ("gqa_hd64", 50, 3),
     ("mha_hd128", 70, 7),
+    ("hd96_kvf32", 41, 5),
+    ("f32w_bf16kv", 36, 4),
 ]
 
 
 @pytest.mark.parametrize("name,L,k", CASES)
 def test_verify_end_to_end(name, L, k):
     shape = S.SHAPES[name]
-    tol = TOL[shape.wdtype]
+    tol = tol_of(shape)
     with Rig(shape, SEED, 1, L + 2 * (k + 1) + 5) as rig:
         prefix = S.prefix_tokens(shape, SEED, 0, L)
         rig.prefill(0, prefix)
@@ -64,7 +66,7 @@ def test_verify_end_to_end(name, L, k):
         assert rig.length(0) == L
 
 
-@pytest.mark.parametrize("name", ["tiny", "ragged_bf16"])
+@pytest.mark.parametrize("name", ["tiny", "ragged_bf16", "hd96_kvf32"])
 def test_prefill_last_logits(name):
     shape = S.SHAPES[name]
     L = 150                      # several 64-row prefill chunks plus a ragged one
@@ -72,8 +74,45 @@ def test_prefill_last_logits(name):
         prefix = S.prefix_tokens(shape, SEED, 0, L)
         z = rig.prefill(0, prefix, want_logits=True)
         zo, _ = forward64(shape, getter(shape), prefix)
-        assert np.abs(z - zo[-1]).max() <= TOL[shape.wdtype]
+        assert np.abs(z - zo[-1]).max() <= tol_of(shape)
         assert rig.length(0) == L
+
+
+# Long caches split every (window, KV head) into several key chunks whose
+# partials the combine launch folds; the chunk size follows the cache's
+# capacity and window count (cdiv(max_len, 512 / (KV heads x query tiles))
+# rounded up to whole workgroup steps):
+#   gqa_hd64, 1 x 1600: 8-wave workgroups, 256-key chunks, 6 chunks, the
+#     last one 26 keys long;
+#   ragged_bf16, 1 x 1600: 5 chunks of 256, 15 query rows in one tile;
+#   gqa_hd64, 8 x 4400: many windows -- 4-wave workgroups with 128-key
+#     chunks (8 chunks), verified on window 5 of the cache;
+#   many_kv, 1 x 6000: 512-key chunks, two 32-key steps per wave;
+#   many_kv, 1 x 9000: 768-key chunks, three steps per wave (two register
+#     sets refilled two steps ahead).
+@pytest.mark.parametrize("name,n_windows,max_len,win,L,k", [
+    ("gqa_hd64", 1, 1600, 0, 1300, 5),
+    ("ragged_bf16", 1, 1600, 0, 1100, 4),
+    ("gqa_hd64", 8, 4400, 5, 1000, 5),
+    ("many_kv", 1, 6000, 0, 1000, 7),
+    ("many_kv", 1, 9000, 0, 1000, 7),
+])
+def test_multichunk_attention(name, n_windows, max_len, win, L, k):
+    shape = S.SHAPES[name]
+    tol = tol_of(shape)
+    with Rig(shape, SEED, n_windows, max_len) as rig:
+        prefix = S.prefix_tokens(shape, SEED, win, L)
+        rig.prefill(win, prefix)
+        wi = S.window_inputs(shape, SEED, 1, k)
+        tokens, q, u = wi["tokens"], wi["q"], wi["u"]
+        out = rig.verify(win, tokens, q, u, commit=True)
+        zo = oracle_logits(shape, prefix, tokens[0])
+        delta = float(np.abs(out["logits"] - zo).max())
+        print(f"{name} {n_windows}x{max_len}: max|dz| = {delta:.3g}")
+        assert delta <= tol
+        split_check(out["logits"], tokens[0], q[0], u[0], out["n"][0], out["token"][0])
+        e2e_check(zo, delta, tokens[0], q[0], u[0], out["n"][0], out["token"][0])
+        assert rig.length(win) == L + out["n"][0] + 1
 
 
 def test_empty_prefix_and_k0():

@@ -23,7 +23,7 @@ from oracle import forward64, greedy64, tree_logits64, tree_walk
 from paper_2405_14105_amd import dsi
 
 from gpu_rig import Rig
-from parity import TOL, getter
+from parity import TOL, getter, tol_of
 
 pytestmark = pytest.mark.gpu
 
@@ -65,10 +65,11 @@ def kv_close(rig, window, shape, cache, n_rows):
             assert err <= rel * float(np.abs(o).max()), (layer, err)
 
 
-@pytest.mark.parametrize("name,L", [("tiny", 40), ("ragged_bf16", 33), ("gqa_hd64", 70)])
+@pytest.mark.parametrize("name,L", [("tiny", 40), ("ragged_bf16", 33), ("gqa_hd64", 70),
+                                    ("hd96_kvf32", 30), ("f32w_bf16kv", 25)])
 def test_tree_matches_oracle_and_commits(name, L):
     shape = S.SHAPES[name]
-    tol = TOL[shape.wdtype]
+    tol = tol_of(shape)
     get = getter(shape, SEED)
     prefix = S.prefix_tokens(shape, SEED, 0, L)
     _, cache = forward64(shape, get, prefix)

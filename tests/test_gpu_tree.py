@@ -65,9 +65,13 @@ def kv_close(rig, window, shape, cache, n_rows):
             assert err <= rel * float(np.abs(o).max()), (layer, err)
 
 
-@pytest.mark.parametrize("name,L", [("tiny", 40), ("ragged_bf16", 33), ("gqa_hd64", 70),
-                                    ("hd96_kvf32", 30), ("f32w_bf16kv", 25)])
-def test_tree_matches_oracle_and_commits(name, L):
+# cap: cache capacity (None: just room for the tree); gqa_hd64 with 1600
+# positions splits the 1200-key prefix into 5 key chunks of 256, so the tree
+# mask meets the chunk partials and their combine
+@pytest.mark.parametrize("name,L,cap", [("tiny", 40, None), ("ragged_bf16", 33, None),
+                                        ("gqa_hd64", 70, None), ("hd96_kvf32", 30, None),
+                                        ("f32w_bf16kv", 25, None), ("gqa_hd64", 1200, 1600)])
+def test_tree_matches_oracle_and_commits(name, L, cap):
     shape = S.SHAPES[name]
     tol = tol_of(shape)
     get = getter(shape, SEED)
@@ -79,7 +83,7 @@ def test_tree_matches_oracle_and_commits(name, L):
     tokens, parent = branchy_tree(w0, g, shape.vocab, rng)
     R = len(tokens)
     zo = tree_logits64(shape, get, cache, tokens, parent)
-    with Rig(shape, SEED, 1, L + 2 * R + 8) as rig:
+    with Rig(shape, SEED, 1, cap or L + 2 * R + 8) as rig:
         rig.prefill(0, prefix)
         out = rig.verify_tree(0, tokens[None], parent[None], commit=True)
         z = out["logits"]

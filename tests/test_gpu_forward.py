@@ -134,12 +134,16 @@ def test_empty_prefix_and_k0():
         assert rig.length(0) == L1 + 1
 
 
-def test_batched_windows_ragged_and_batch_invariant():
+# lens, cache capacity: one key chunk; or 256-key chunks over a 1250-key
+# prefix, where the 40-key window's later chunks hold no key at all (their
+# partials carry max -inf and sum 0) and alone it takes the single-chunk
+# path that normalises inside the attention kernel
+@pytest.mark.parametrize("lens,cap", [([20, 33, 47, 5], 64), ([300, 1250, 40], 1600)])
+def test_batched_windows_ragged_and_batch_invariant(lens, cap):
     shape = S.SHAPES["gqa_hd64"]
-    lens = [20, 33, 47, 5]
     k = 4
     B = len(lens)
-    with Rig(shape, SEED, B, 64) as rig:
+    with Rig(shape, SEED, B, cap) as rig:
         prefixes = [S.prefix_tokens(shape, SEED, b, lens[b]) for b in range(B)]
         for b in range(B):
             rig.prefill(b, prefixes[b])

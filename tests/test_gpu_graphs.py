@@ -60,14 +60,20 @@ def run(rig, buf, window0, B, k, mode, commit):
     return buf.z.cpu().numpy().copy(), buf.n.cpu().numpy().copy(), buf.t.cpu().numpy().copy()
 
 
-@pytest.mark.parametrize("name", ["ragged_bf16", "gqa_hd64"])
-def test_graph_replays_match_eager(name):
+# lens, cache capacity: one key chunk; or 256-key chunks with the chunk
+# launch and the combine inside the graph, the longest window 1010 keys so
+# that commits take its key range past 1024 (a fifth chunk: a new plan and
+# a new graph) between replays
+@pytest.mark.parametrize("name,lens,cap", [("ragged_bf16", [17, 40, 29], 200),
+                                           ("gqa_hd64", [17, 40, 29], 200),
+                                           ("gqa_hd64", [300, 1010, 250], 1600)])
+def test_graph_replays_match_eager(name, lens, cap):
     shape = S.SHAPES[name]
-    B, lens = 3, [17, 40, 29]
+    B = len(lens)
     side = torch.cuda.Stream()
     with torch.cuda.stream(side):
-        eager = make_rig(shape, False, B, 200)
-        graph = make_rig(shape, True, B, 200)
+        eager = make_rig(shape, False, B, cap)
+        graph = make_rig(shape, True, B, cap)
         try:
             for b in range(B):
                 p = S.prefix_tokens(shape, SEED, b, lens[b])

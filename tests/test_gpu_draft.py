@@ -41,11 +41,14 @@ def run_draft(rig, window, feed, k, u, temperature=1.0):
     return tok.cpu().numpy(), q.cpu().numpy()
 
 
-@pytest.mark.parametrize("target,T", [("tiny", 1.0), ("ragged_bf16", 1.0), ("tiny", 0.7)])
-def test_draft_rows_and_draws(target, T):
+# L, cap: a short context; or a 1500-token context in a 2000-position
+# cache, whose single-row draft steps then read 6 key chunks of 256
+@pytest.mark.parametrize("target,T,L,cap", [("tiny", 1.0, 40, None), ("ragged_bf16", 1.0, 40, None),
+                                            ("tiny", 0.7, 40, None), ("ragged_bf16", 1.0, 1500, 2000)])
+def test_draft_rows_and_draws(target, T, L, cap):
     ds = S.SHAPES[S.DRAFTERS[target]]
-    L, k = 40, 6
-    with Rig(ds, DSEED, 1, L + 2 * k + 4) as rig:
+    k = 6
+    with Rig(ds, DSEED, 1, cap or L + 2 * k + 4) as rig:
         prefix = S.prefix_tokens(ds, SEED, 0, L)
         rig.prefill(0, prefix)
         rng = np.random.default_rng(7)

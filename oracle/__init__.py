@@ -14,8 +14,10 @@ from it; the product path never calls it.
 Parity status of each function (what pins it) is listed in its docstring.
 Architecture choices of the forward (RMSNorm, rotate-half RoPE, GQA head
 grouping, SwiGLU, untied head) are not fixed by the paper, which treats the
-target LM as a black box (Appendix B); they are pinned here only by invariants
-and textbook special cases -- "parity unpinned" beyond those.
+target LM as a black box (Appendix B); they are pinned by invariants, textbook
+special cases and, for the whole decoder, by an independent implementation of
+the same architecture (the transformers library's Llama model, loaded with
+the same weights, in a CPU test).
 """
 from .model import (bf16_round64, rmsnorm64, rope64, attention64, silu64,
                         layer64, head64, forward64, embed64)

@@ -209,3 +209,48 @@ def test_layer_by_layer_equals_forward():
         np.testing.assert_array_equal(x, hid[l + 1])
         np.testing.assert_array_equal(kn, cache[l][0])
     np.testing.assert_array_equal(head64(s, get, hid[-1]), z)
+
+
+# ------------------------------------- whole decoder against an independent Llama
+_HF_NAMES = {"attn_norm": "input_layernorm.weight", "wq": "self_attn.q_proj.weight",
+             "wk": "self_attn.k_proj.weight", "wv": "self_attn.v_proj.weight",
+             "wo": "self_attn.o_proj.weight", "ffn_norm": "post_attention_layernorm.weight",
+             "w_gate": "mlp.gate_proj.weight", "w_up": "mlp.up_proj.weight",
+             "w_down": "mlp.down_proj.weight"}
+
+
+@pytest.mark.parametrize("name", ["tiny", "ragged_bf16", "gqa_hd64"])
+def test_forward_matches_transformers_llama(name):
+    """The whole decoder the oracle states (pre-norm RMSNorm, rotate-half
+    RoPE, GQA head grouping, SwiGLU, final norm, untied head) against the
+    transformers library's Llama model built from a config (random init, no
+    download), loaded with the same synthetic weights and run in fp64 with
+    eager attention, causal over a 37-token sequence.  The library keeps
+    its RMSNorm in fp32, hence the 1e-6 bound (measured ~1.4e-7)."""
+    transformers = pytest.importorskip("transformers")
+    import dataclasses
+    s = S.SHAPES[name]
+    cfg = transformers.LlamaConfig(
+        vocab_size=s.vocab, hidden_size=s.d_model, intermediate_size=s.d_ff,
+        num_hidden_layers=s.n_layers, num_attention_heads=s.n_heads,
+        num_key_value_heads=s.n_kv_heads, head_dim=s.head_dim, rms_norm_eps=s.rms_eps,
+        rope_theta=s.rope_base, max_position_embeddings=1024, tie_word_embeddings=False,
+        attention_bias=False, mlp_bias=False, hidden_act="silu")
+    cfg._attn_implementation = "eager"
+    torch.manual_seed(0)
+    model = transformers.LlamaForCausalLM(cfg).double().eval()
+    get = getter(s)
+    sd = {"model.embed_tokens.weight": get(-1, "embed"), "model.norm.weight": get(-1, "final_norm"),
+          "lm_head.weight": get(-1, "lm_head")}
+    for l in range(s.n_layers):
+        for ours, theirs in _HF_NAMES.items():
+            sd[f"model.layers.{l}.{theirs}"] = get(l, ours)
+    model.load_state_dict({k: torch.from_numpy(np.ascontiguousarray(v)) for k, v in sd.items()}, strict=True)
+    toks = S.prefix_tokens(s, 0, 0, 37)
+    with torch.no_grad():
+        zh = model(torch.from_numpy(np.asarray(toks, np.int64))[None]).logits[0].numpy()
+    # the oracle with an fp32 cache: no bf16 rounding of K/V (the library has none)
+    zo, _ = forward64(dataclasses.replace(s, kvdtype="f32"), get, toks)
+    err = float(np.abs(zh - zo).max())
+    print(f"{name}: max |z_oracle - z_transformers| = {err:.3g}")
+    assert err <= 1e-6 * max(1.0, float(np.abs(zo).max()))

@@ -89,13 +89,16 @@ def test_prefill_last_logits(name):
 #     chunks (8 chunks), verified on window 5 of the cache;
 #   many_kv, 1 x 6000: 512-key chunks, two 32-key steps per wave;
 #   many_kv, 1 x 9000: 768-key chunks, three steps per wave (two register
-#     sets refilled two steps ahead).
+#     sets refilled two steps ahead);
+#   tiny (fp32 cache), 8 x 2100: the many-window 4-wave plan on an fp32
+#     cache (128-key chunks), window 3.
 @pytest.mark.parametrize("name,n_windows,max_len,win,L,k", [
     ("gqa_hd64", 1, 1600, 0, 1300, 5),
     ("ragged_bf16", 1, 1600, 0, 1100, 4),
     ("gqa_hd64", 8, 4400, 5, 1000, 5),
     ("many_kv", 1, 6000, 0, 1000, 7),
     ("many_kv", 1, 9000, 0, 1000, 7),
+    ("tiny", 8, 2100, 3, 900, 5),
 ])
 def test_multichunk_attention(name, n_windows, max_len, win, L, k):
     shape = S.SHAPES[name]

@@ -91,7 +91,9 @@ def test_prefill_last_logits(name):
 #   many_kv, 1 x 9000: 768-key chunks, three steps per wave (two register
 #     sets refilled two steps ahead);
 #   tiny (fp32 cache), 8 x 2100: the many-window 4-wave plan on an fp32
-#     cache (128-key chunks), window 3.
+#     cache (128-key chunks), window 3;
+#   tiny (fp32 cache), 1 x 33000: 512-key chunks, two steps per wave on
+#     fp32 keys and values.
 @pytest.mark.parametrize("name,n_windows,max_len,win,L,k", [
     ("gqa_hd64", 1, 1600, 0, 1300, 5),
     ("ragged_bf16", 1, 1600, 0, 1100, 4),
@@ -99,6 +101,7 @@ def test_prefill_last_logits(name):
     ("many_kv", 1, 6000, 0, 1000, 7),
     ("many_kv", 1, 9000, 0, 1000, 7),
     ("tiny", 8, 2100, 3, 900, 5),
+    ("tiny", 1, 33000, 0, 700, 5),
 ])
 def test_multichunk_attention(name, n_windows, max_len, win, L, k):
     shape = S.SHAPES[name]

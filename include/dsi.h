@@ -120,8 +120,17 @@ dsi_status dsi_kv_destroy(dsi_kv* kv);
 
 /* Append n prompt tokens (d_tokens [n], device) to a window: runs the target
  * over them in chunks, writes their K/V, and advances the window length by n.
- * d_last_logits (nullable, device [V] fp32) receives the logits of the last
- * token.  Fails with DSI_ECAPACITY if length + n may exceed max_len. */
+ * This builds the committed prefix a target server keeps in its own KV cache
+ * (Section 3.1, "KV cache"): the prompt x of the target's next-token model
+ * f(x) (Appendix B, the unpadded prompt with positions from 0), and also
+ * tokens a server must catch up on before verifying (committed tokens or the
+ * drafts a task builds on).  d_last_logits (nullable, device [V] fp32)
+ * receives the logits of the last token.  Fails with DSI_ECAPACITY if
+ * length + n may exceed max_len, with no side effects.  The tokens run in
+ * chunks of DSI_MAX_ROWS; a chunk holding an id outside [0, V) does not
+ * advance the length and is reported by the next synchronising call
+ * (DSI_EINVAL).  Stream-ordered; d_tokens is caller-owned and only read by
+ * the call's stream work. */
 dsi_status dsi_prefill(dsi_model* m, dsi_kv* kv, int32_t window, const int32_t* d_tokens,
                        int32_t n, float* d_last_logits);
 

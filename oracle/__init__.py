@@ -21,7 +21,7 @@ the same weights, in a CPU test).
 """
 from .model import (bf16_round64, rmsnorm64, rope64, attention64, silu64,
                         layer64, head64, forward64, embed64)
-from .verification import VerifyResult, softmax64, verify64, verify64_batch
+from .verification import VerifyResult, softmax64, verify64
 from . import bruteforce
 from .drafting import DraftResult, draft64, draft_q32, draw_inverse_cdf, si_loop64
 from .tree import ancestors, greedy64, tree_logits64, tree_walk, validate_tree
@@ -29,6 +29,6 @@ from .tree import ancestors, greedy64, tree_logits64, tree_walk, validate_tree
 __all__ = [
     "bf16_round64", "rmsnorm64", "rope64", "attention64", "silu64", "layer64",
     "head64", "forward64", "embed64", "VerifyResult", "softmax64", "verify64",
-    "verify64_batch", "bruteforce", "DraftResult", "draft64", "draft_q32", "draw_inverse_cdf",
+    "bruteforce", "DraftResult", "draft64", "draft_q32", "draw_inverse_cdf",
     "si_loop64", "ancestors", "greedy64", "tree_logits64", "tree_walk", "validate_tree",
 ]

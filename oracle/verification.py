@@ -118,17 +118,3 @@ def verify64(z, drafts, q=None, u=None, temperature: float = 1.0, mode: str = "s
     bounds = np.concatenate([[0.0], c])
     draw_margin = float(np.min(np.abs(bounds - target)) / R)
     return VerifyResult(n, token, mode, a, accept_margin, draw_margin, r, R)
-
-
-def verify64_batch(z, tokens, q, u, temperature: float = 1.0, mode: str = "sample"):
-    """verify64 over B windows: z [B*(k+1), V] (window-major), tokens [B, k+1]
-    = (w0, d_1..d_k), q [B, k, V], u [B, k+1].  Returns a list of results."""
-    tokens = np.asarray(tokens)
-    B, k1 = tokens.shape
-    z = np.asarray(z).reshape(B, k1, -1)
-    out = []
-    for b in range(B):
-        out.append(verify64(z[b], tokens[b, 1:],
-                            None if q is None else q[b],
-                            None if u is None else u[b], temperature, mode))
-    return out

@@ -138,7 +138,14 @@ class DsiExecutor:
                 dsi.dsi_verify(self.target, srv.kv, s, 1, len(window) - 1, tk, None, None,
                                self.n_out, self.t_out, 1.0, dsi.DSI_GREEDY, True)
                 n, tok = int(self.n_out.item()), int(self.t_out.item())
+                if n < 0:
+                    raise RuntimeError("verification reported an input error")
                 srv.toks += window[:n + 1]
+                # the host's bound on the server's length grew by the window's
+                # row count; reading the length (the stream is idle after the
+                # reads above) tightens it to the committed L + n + 1
+                if dsi.dsi_kv_length(srv.kv, s) != srv.base + len(srv.toks):
+                    raise RuntimeError("server cache length disagrees with its committed tokens")
                 remaining = N - (len(committed) - 1)
                 if n < len(window) - 1:                  # draft checked + 1 + n rejected
                     r = checked + 1 + n

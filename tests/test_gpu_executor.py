@@ -2,7 +2,12 @@
 exact-match verification DSI returns exactly the target's own greedy tokens
 (Theorem 1: the same output as the target alone), whatever the drafter, the
 lookahead and the number of target servers; and its simulated wall time is
-never above non-SI's."""
+never above non-SI's.
+
+"The target's own greedy tokens" are taken from the oracle (an fp64 forward
+per step, tests/parity.py::oracle_greedy_continuation): every token whose
+top-2 logit gap exceeds twice the fp32 logit tolerance must match exactly,
+and the tokens also match the GPU's own one-token-per-forward decode."""
 import numpy as np
 import pytest
 import torch
@@ -12,6 +17,7 @@ from paper_2405_14105_amd import dsi
 from paper_2405_14105_amd.executor import DsiExecutor
 
 from gpu_rig import Rig
+from parity import oracle_greedy_continuation
 
 pytestmark = pytest.mark.gpu
 
@@ -47,10 +53,39 @@ def test_dsi_returns_the_target_greedy_tokens(drafter, T, k, sp):
                          t_target=1.0, t_drafter=0.1, draft_temperature=T, seed=3)
         run = ex.generate(w0, N)
         ref = greedy_reference(trig, sp, w0, N)
+    ora, sure = oracle_greedy_continuation(ts, prompt, w0, N, seed=SEED)
     print(f"{drafter} k={k} sp={sp}: {run.tasks} tasks, {run.rejections} rejections, "
-          f"simulated time {run.time:.2f} (non-SI {N * 1.0:.0f})")
+          f"simulated time {run.time:.2f} (non-SI {N * 1.0:.0f}); oracle-decided tokens {sure}/{N}")
+    assert sure >= N // 2
+    assert run.tokens[:sure] == ora[:sure]
     assert run.tokens == ref
     assert run.time <= N * 1.0 + 1e-9
+
+
+def test_dsi_long_generation_keeps_the_length_bound_tight():
+    """200 tokens through 3 servers whose caches have room for the prompt,
+    the output and two windows only: every committed verification must
+    leave the host's length bound at the real length (it grows by the
+    window's k + 1 rows per call otherwise, and a later call would fail with
+    a false capacity error)."""
+    ts = S.SHAPES["tiny"]
+    L, N, w0, k, sp = 30, 200, 11, 4, 3
+    cap = L + N + 2 * (k + 1)
+    prompt = S.prefix_tokens(ts, SEED, 0, L)
+    with Rig(ts, SEED, sp + 1, cap) as trig, Rig(ts, SEED, 1, cap + k) as drig:
+        for s in range(sp + 1):
+            trig.prefill(s, prompt)
+        drig.prefill(0, prompt)
+        ex = DsiExecutor(trig.model, trig.kv, drig.model, drig.kv, ts.vocab, k, sp, L,
+                         draft_temperature=0.05, seed=7)
+        run = ex.generate(w0, N)
+        lens = [trig.length(s) for s in range(sp)]
+    ora, sure = oracle_greedy_continuation(ts, prompt, w0, N, seed=SEED)
+    print(f"N={N}: {run.tasks} tasks, {run.rejections} rejections, server lengths {lens}, "
+          f"oracle-decided tokens {sure}/{N}")
+    assert all(Lb <= cap for Lb in lens)
+    assert sure >= N // 4
+    assert run.tokens[:sure] == ora[:sure]
 
 
 @pytest.mark.parametrize("drafters,k", [(("tiny_draft",), 3), (("tiny_draft", "same"), 3),
@@ -83,7 +118,11 @@ def test_tree_executor_returns_the_target_greedy_tokens(drafters, k):
     finally:
         for r in rigs:
             r.close()
-    print(f"{drafters} k={k}: {run.forwards} target forwards for {N} tokens, accepted {run.accepted}")
+    ora, sure = oracle_greedy_continuation(ts, prompt, w0, N, seed=SEED)
+    print(f"{drafters} k={k}: {run.forwards} target forwards for {N} tokens, accepted {run.accepted}; "
+          f"oracle-decided tokens {sure}/{N}")
+    assert sure >= N // 2
+    assert run.tokens[:sure] == ora[:sure]
     assert run.tokens == ref
     assert run.forwards <= N
     if "same" in drafters:

@@ -3,11 +3,16 @@ small models that span several MFMA tiles with ragged tails (vocab, d_ff,
 query tiles, key chunks).
 
 Gates:
-  * logits: max |z_gpu - z_oracle| <= 1e-4 (fp32 models) or 2e-2 (bf16);
+  * logits: max |z_gpu - z_oracle| <= 1e-4 (fp32 models) or 2e-2 (bf16),
+    the contract tolerances, and the regression gate of the shape (about ten
+    times the error measured on it, tests/parity.py REG);
   * split check: the GPU's accept/reject on its own logits equals the
     oracle's verification of those same logits (flagged positions excluded);
   * end-to-end: equal to the oracle's verification of the oracle's logits
-    except where the logit error delta could flip a decision;
+    except where the logit error delta could flip a decision; the single
+    window tests take uniforms settled on the oracle's side (no decision
+    within reach of the regression gate) and assert that both checks
+    compared the decisions;
   * KV state: committed length L + n + 1, rollback, batch invariance.
 """
 import numpy as np
@@ -19,7 +24,7 @@ from oracle import forward64
 from paper_2405_14105_amd import dsi
 
 from gpu_rig import Rig
-from parity import TOL, e2e_check, getter, oracle_logits, split_check, tol_of
+from parity import TOL, e2e_check, getter, oracle_logits, reg_of, settle_u, split_check, tol_of
 
 pytestmark = pytest.mark.gpu
 
@@ -40,29 +45,31 @@ CASES = [
 @pytest.mark.parametrize("name,L,k", CASES)
 def test_verify_end_to_end(name, L, k):
     shape = S.SHAPES[name]
-    tol = tol_of(shape)
+    tol, reg = tol_of(shape), reg_of(shape)
+    prefix = S.prefix_tokens(shape, SEED, 0, L)
+    wi = S.window_inputs(shape, SEED, 1, k)
+    tokens, q = wi["tokens"], wi["q"]
+    zo, ho = oracle_logits(shape, prefix, tokens[0], return_hidden=True)
+    u = settle_u(zo, tokens[0], q[0], wi["u"][0], reg)[None]
     with Rig(shape, SEED, 1, L + 2 * (k + 1) + 5) as rig:
-        prefix = S.prefix_tokens(shape, SEED, 0, L)
         rig.prefill(0, prefix)
         assert rig.length(0) == L
-        wi = S.window_inputs(shape, SEED, 1, k)
-        tokens, q, u = wi["tokens"], wi["q"], wi["u"]
         out = rig.verify(0, tokens, q, u, commit=True, want_hidden=True)
-        zo, ho = oracle_logits(shape, prefix, tokens[0], return_hidden=True)
         per_layer = [float(np.abs(out["hidden"][l] - ho[l]).max()) for l in range(shape.n_layers + 1)]
         delta = float(np.abs(out["logits"] - zo).max())
-        print(f"{name}: max|dz| = {delta:.3g}; hidden max err per layer {per_layer}")
-        assert delta <= tol
-        split_check(out["logits"], tokens[0], q[0], u[0], out["n"][0], out["token"][0])
-        e2e_check(zo, delta, tokens[0], q[0], u[0], out["n"][0], out["token"][0])
+        print(f"{name}: max|dz| = {delta:.3g} (gate {reg:g}); hidden max err per layer {per_layer}")
+        assert delta <= tol and delta <= reg
+        assert split_check(out["logits"], tokens[0], q[0], u[0], out["n"][0], out["token"][0]) is not None
+        assert e2e_check(zo, delta, tokens[0], q[0], u[0], out["n"][0], out["token"][0]) is not None
         assert 0 <= out["n"][0] <= k
         assert rig.length(0) == L + out["n"][0] + 1
         # greedy on the same window after rolling back: identical logits
         dsi.dsi_kv_rollback(rig.kv, 0, L)
         g = rig.verify(0, tokens, mode=dsi.DSI_GREEDY, commit=False)
         assert np.array_equal(g["logits"], out["logits"])
-        split_check(g["logits"], tokens[0], None, None, g["n"][0], g["token"][0], mode="greedy")
-        e2e_check(zo, delta, tokens[0], None, None, g["n"][0], g["token"][0], mode="greedy")
+        assert split_check(g["logits"], tokens[0], None, None, g["n"][0], g["token"][0],
+                           mode="greedy") is not None
+        assert e2e_check(zo, delta, tokens[0], None, None, g["n"][0], g["token"][0], mode="greedy") is not None
         assert rig.length(0) == L
 
 
@@ -74,7 +81,9 @@ def test_prefill_last_logits(name):
         prefix = S.prefix_tokens(shape, SEED, 0, L)
         z = rig.prefill(0, prefix, want_logits=True)
         zo, _ = forward64(shape, getter(shape), prefix)
-        assert np.abs(z - zo[-1]).max() <= tol_of(shape)
+        d = float(np.abs(z - zo[-1]).max())
+        print(f"{name}: prefill last-row max|dz| = {d:.3g}")
+        assert d <= tol_of(shape) and d <= reg_of(shape)
         assert rig.length(0) == L
 
 
@@ -105,19 +114,20 @@ def test_prefill_last_logits(name):
 ])
 def test_multichunk_attention(name, n_windows, max_len, win, L, k):
     shape = S.SHAPES[name]
-    tol = tol_of(shape)
+    tol, reg = tol_of(shape), reg_of(shape)
+    prefix = S.prefix_tokens(shape, SEED, win, L)
+    wi = S.window_inputs(shape, SEED, 1, k)
+    tokens, q = wi["tokens"], wi["q"]
+    zo = oracle_logits(shape, prefix, tokens[0])
+    u = settle_u(zo, tokens[0], q[0], wi["u"][0], reg)[None]
     with Rig(shape, SEED, n_windows, max_len) as rig:
-        prefix = S.prefix_tokens(shape, SEED, win, L)
         rig.prefill(win, prefix)
-        wi = S.window_inputs(shape, SEED, 1, k)
-        tokens, q, u = wi["tokens"], wi["q"], wi["u"]
         out = rig.verify(win, tokens, q, u, commit=True)
-        zo = oracle_logits(shape, prefix, tokens[0])
         delta = float(np.abs(out["logits"] - zo).max())
-        print(f"{name} {n_windows}x{max_len}: max|dz| = {delta:.3g}")
-        assert delta <= tol
-        split_check(out["logits"], tokens[0], q[0], u[0], out["n"][0], out["token"][0])
-        e2e_check(zo, delta, tokens[0], q[0], u[0], out["n"][0], out["token"][0])
+        print(f"{name} {n_windows}x{max_len}: max|dz| = {delta:.3g} (gate {reg:g})")
+        assert delta <= tol and delta <= reg
+        assert split_check(out["logits"], tokens[0], q[0], u[0], out["n"][0], out["token"][0]) is not None
+        assert e2e_check(zo, delta, tokens[0], q[0], u[0], out["n"][0], out["token"][0]) is not None
         assert rig.length(win) == L + out["n"][0] + 1
 
 
@@ -160,7 +170,7 @@ def test_batched_windows_ragged_and_batch_invariant(lens, cap):
         for b in range(B):
             zo = oracle_logits(shape, prefixes[b], wi["tokens"][b])
             delta = float(np.abs(zz[b] - zo).max())
-            assert delta <= TOL["bf16"], (b, delta)
+            assert delta <= TOL["bf16"] and delta <= reg_of(shape), (b, delta)
             split_check(zz[b], wi["tokens"][b], wi["q"][b], wi["u"][b], out["n"][b], out["token"][b])
         # each window alone gives bit-identical logits and decisions
         for b in range(B):
@@ -257,8 +267,9 @@ def test_many_key_chunks_end_to_end(name):
     zo = oracle_logits(shape, prefix, wi["tokens"][0])
     delta = float(np.abs(out["logits"] - zo).max())
     print(f"{name}: L = {L}, max|dz| = {delta:.3g}")
-    assert delta <= tol
-    split_check(out["logits"], wi["tokens"][0], None, None, out["n"][0], out["token"][0], mode="greedy")
+    assert delta <= tol and delta <= reg_of(shape)
+    assert split_check(out["logits"], wi["tokens"][0], None, None, out["n"][0], out["token"][0],
+                       mode="greedy") is not None
 
 
 def test_verify_at_the_row_maximum():
@@ -280,5 +291,5 @@ def test_verify_at_the_row_maximum():
             assert np.array_equal(one["logits"], z[b])
     for b in range(B):
         zo = oracle_logits(shape, prefixes[b], wi["tokens"][b])
-        assert np.abs(z[b] - zo).max() <= TOL["f32"], b
+        assert np.abs(z[b] - zo).max() <= min(TOL["f32"], reg_of(shape)), b
         split_check(z[b], wi["tokens"][b], wi["q"][b], wi["u"][b], out["n"][b], out["token"][b])

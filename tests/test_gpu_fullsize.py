@@ -15,9 +15,16 @@ one, teacher-forced on the GPU's own state:
   * KV state: commit length, rollback and bit-identical re-verification,
     batch invariance of the 7-window batch.
 The 1B shape is checked end to end: the oracle's full forward over the prefix
-and window against the GPU's logits.
+and window against the GPU's logits.  At the 8B shape the oracle's window
+logits were computed once by tests/golden/make_fullsize_logits.py (fp64,
+32 layers over the whole prefix + window, minutes on a CPU) and stored; the
+GPU's logits are compared with them element by element (the 2e-2 contract
+for bf16 logits) and the accept/reject decisions with the oracle's
+decisions on them, for the one-window workload and two windows of the
+seven-window batch.
 """
 import copy
+import os
 import time
 
 import numpy as np
@@ -29,7 +36,7 @@ from oracle import ancestors, head64, layer64, softmax64, tree_walk
 from paper_2405_14105_amd import dsi
 
 from gpu_rig import Rig
-from parity import TOL, e2e_check, getter, oracle_logits, split_check
+from parity import TOL, e2e_check, e2e_check_parts, getter, oracle_logits, settle_u, split_check
 
 pytestmark = [pytest.mark.gpu, pytest.mark.fullsize, pytest.mark.timeout(900)]
 
@@ -98,29 +105,41 @@ def check_verify(logits, tokens, q, u, n, tok, k, mode="sample"):
 
 
 # ----------------------------------------------------------------- 1B, L 512, k 5
+# 1B end to end: measured max |dz| 1.8-1.9e-3 (the bf16 KV rounding cascade
+# over 16 layers); the regression gate sits below the 2e-2 contract
+REG_1B = 5e-3
+
+
 def test_1b_L512_k5_end_to_end():
     shape = S.SHAPES["llama1b"]
     L, k = 512, 5
     t0 = time.time()
+    prefix = S.prefix_tokens(shape, SEED, 0, L)
+    wi = S.window_inputs(shape, SEED, 1, k)
+    toks, q = wi["tokens"], wi["q"]
+    zo = oracle_logits(shape, prefix, toks[0], seed=SEED, cache=False)
+    say(f"  1B oracle done ({time.time() - t0:.1f}s)")
+    u = settle_u(zo, toks[0], q[0], wi["u"][0], REG_1B)[None]
     with Rig(shape, SEED, 1, L + 2 * (k + 1)) as rig:
-        prefix = S.prefix_tokens(shape, SEED, 0, L)
         rig.prefill(0, prefix)
-        wi = S.window_inputs(shape, SEED, 1, k)
-        toks, q, u = wi["tokens"], wi["q"], wi["u"]
         out = rig.verify(0, toks, q, u, commit=True)
         assert rig.length(0) == L + out["n"][0] + 1
         dsi.dsi_kv_rollback(rig.kv, 0, L)
         g = rig.verify(0, toks, mode=dsi.DSI_GREEDY, commit=False)
         assert np.array_equal(g["logits"], out["logits"])
     say(f"  GPU done ({time.time() - t0:.1f}s)")
-    zo = oracle_logits(shape, prefix, toks[0], seed=SEED, cache=False)
     delta = float(np.abs(out["logits"] - zo).max())
     say(f"  1B end to end: max|dz| = {delta:.3g} ({time.time() - t0:.1f}s)")
-    assert delta <= TOL["bf16"]
-    check_verify(out["logits"], toks[0], q[0], u[0], out["n"][0], out["token"][0], k)
-    e2e_check(zo, delta, toks[0], q[0], u[0], out["n"][0], out["token"][0])
-    check_verify(g["logits"], toks[0], None, None, g["n"][0], g["token"][0], k, mode="greedy")
-    e2e_check(zo, delta, toks[0], None, None, g["n"][0], g["token"][0], mode="greedy")
+    assert delta <= TOL["bf16"] and delta <= REG_1B
+    assert check_verify(out["logits"], toks[0], q[0], u[0], out["n"][0], out["token"][0], k) is not None
+    assert check_verify(g["logits"], toks[0], None, None, g["n"][0], g["token"][0], k, mode="greedy") is not None
+    # end to end at this delta the sampled draw over 32000 entries is within
+    # reach of the logit error (no uniform gets a 4 delta CDF margin), so the
+    # accepted count is compared on its own; greedy compares both
+    ns, ts = e2e_check_parts(zo, delta, toks[0], q[0], u[0], out["n"][0], out["token"][0])
+    ng, tg = e2e_check_parts(zo, delta, toks[0], None, None, g["n"][0], g["token"][0], mode="greedy")
+    say(f"  1B compared with the oracle's decisions: sampling n {ns} token {ts}; greedy n {ng} token {tg}")
+    assert ns and ng and tg
 
 
 # ------------------------------------------------- 8B: one window L 2048 k 10, and 7 windows
@@ -161,7 +180,7 @@ def test_8b_L2048_k10_layers_head_and_verify(rig8b):
     out = rig.verify(0, toks, q, u, commit=False, want_hidden=True)
     hid, z = out["hidden"], out["logits"]
     rows = np.arange(K8 + 1)
-    for layer in (0, shape.n_layers // 2, shape.n_layers - 1):
+    for layer in range(shape.n_layers):
         check_layer(rig, shape, 0, layer, L8, hid, rows)
     check_head(shape, hid[shape.n_layers], z, rows)
     check_verify(z, toks[0], q[0], u[0], out["n"][0], out["token"][0], K8)
@@ -169,6 +188,60 @@ def test_8b_L2048_k10_layers_head_and_verify(rig8b):
     assert np.array_equal(g["logits"], z)
     check_verify(z, toks[0], None, None, g["n"][0], g["token"][0], K8, mode="greedy")
     assert rig.length(0) == L8
+
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def fixture_logits(case):
+    f = np.load(os.path.join(GOLDEN, f"{case}_logits.npz"))
+    return {k: f[k] for k in f.files}
+
+
+def end_to_end_8b(z, fx, toks, q, u, n, tok, g, label):
+    """Element-wise logits against the stored oracle rows, then the oracle's
+    decisions on those rows against the GPU's (sampling and greedy)."""
+    zo = fx["logits"].astype(np.float64)
+    assert np.array_equal(fx["tokens"], toks), label
+    d = np.abs(z - zo)
+    delta = float(d.max())
+    say(f"  {label}: end-to-end max|dz| = {delta:.4g} (row maxima {np.round(d.max(axis=1), 4).tolist()}, "
+        f"mean {float(d.mean()):.3g}); logit std {float(zo.std()):.3g}")
+    assert delta <= TOL["bf16"], (label, delta)
+    ns, ts = e2e_check_parts(zo, delta, toks, q, u, n, tok)
+    ng, tg = e2e_check_parts(zo, delta, toks, None, None, g["n"], g["token"], mode="greedy")
+    say(f"  {label}: compared with the oracle's decisions: sampling n {ns} token {ts}; "
+        f"greedy n {ng} token {tg}")
+    assert ns and ng, label
+    return delta
+
+
+def test_8b_end_to_end_against_oracle_fixture(rig8b):
+    """The 8B window logits against the fp64 oracle's, end to end: one
+    window (prefix 2048, k 10) and windows 0 and 6 of the seven-window batch
+    (prefixes 1024 and 1030, k 5), on the caches and launch plans the
+    benchmark times."""
+    shape = rig8b.shape
+    fx = fixture_logits("llama8b_L2048_k10_w0")
+    wi = S.window_inputs(shape, SEED, 1, K8)
+    toks, q = wi["tokens"], wi["q"]
+    u = settle_u(fx["logits"].astype(np.float64), toks[0], q[0], wi["u"][0], 2e-2)[None]
+    out = rig8b.verify(0, toks, q, u, commit=False)
+    g = rig8b.verify(0, toks, mode=dsi.DSI_GREEDY, commit=False)
+    end_to_end_8b(out["logits"], fx, toks[0], q[0], u[0], out["n"][0], out["token"][0],
+                  {"n": g["n"][0], "token": g["token"][0]}, "8B L2048 k10")
+    rig, B, k = rig8b.rig7, len(LENS7), K7
+    wi = S.window_inputs(shape, SEED, B, k)
+    toks, q, u = wi["tokens"], wi["q"], wi["u"].copy()
+    fxs = {b: fixture_logits(f"llama8b_x7_L1024_k5_w{b}") for b in (0, B - 1)}
+    for b, f in fxs.items():
+        u[b] = settle_u(f["logits"].astype(np.float64), toks[b], q[b], u[b], 2e-2)
+    out = rig.verify(0, toks, q, u, commit=False)
+    g = rig.verify(0, toks, mode=dsi.DSI_GREEDY, commit=False)
+    zz = out["logits"].reshape(B, k + 1, shape.vocab)
+    for b, f in fxs.items():
+        end_to_end_8b(zz[b], f, toks[b], q[b], u[b], out["n"][b], out["token"][b],
+                      {"n": g["n"][b], "token": g["token"][b]}, f"8B x7 window {b} (L {LENS7[b]}, k 5)")
 
 
 def test_8b_L2048_k10_bonus_commit_rollback(rig8b):

@@ -238,6 +238,24 @@ dsi_status dsi_accept(void* stream, int32_t n_windows, int32_t k, int32_t vocab,
                       const float* d_u, float temperature, int32_t mode,
                       int32_t* d_n_accepted, int32_t* d_next_token);
 
+/* dsi_accept without any device allocation, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc.  Same arguments, kernels and results as
+ * dsi_accept (n and the token equal dsi_accept's on the same inputs).  Its
+ * workspace is one fixed device array of DSI_ACCEPT_NOALLOC_BYTES per device
+ * (256 bytes of it the error word), held from the first call on a device
+ * until the process ends; no hipMalloc/hipFree is called.  A call whose
+ * n_windows*(k+1) rows and vocabulary need more workspace than the array
+ * holds fails with DSI_ECAPACITY before anything is enqueued (128256-entry
+ * vocabularies fit at the 64-row maximum).  Every call on a device shares
+ * that device's array: calls that overlap on one device (other streams,
+ * other threads) race and must be serialised by the caller. */
+#define DSI_ACCEPT_NOALLOC_BYTES (256 * 1024)
+dsi_status dsi_accept_noalloc(void* stream, int32_t n_windows, int32_t k, int32_t vocab,
+                              const float* d_logits, const int32_t* d_tokens, const float* d_q,
+                              const float* d_u, float temperature, int32_t mode,
+                              int32_t* d_n_accepted, int32_t* d_next_token);
+
 /* Roll a window back to new_len (DSI terminates the threads that built on a
  * rejected token, Algorithm 1; their cache rows become dead).  Stream-ordered;
  * new_len must be >= 0 and not above the window's current length (checked on

@@ -573,6 +573,36 @@ dsi_status replay_or_capture(dsi_model* m, const std::vector<uint64_t>& key, F&&
   return DSI_OK;
 }
 
+// ---------------------------------------------------------------- no-alloc accept
+// Fixed device array holding the accept/reject workspace of
+// dsi_accept_noalloc: the first 256 bytes are the device error word, the
+// rest the verification workspace.  Each device holds its own copy at its own
+// address until the process ends.  In host code `scratch` names a host-side
+// stand-in, so kernels and fills only ever see the device address taken by
+// hipGetSymbolAddress below.
+constexpr size_t kScratchHead = 256;
+static __device__ __align__(256) unsigned char scratch[DSI_ACCEPT_NOALLOC_BYTES];
+std::mutex g_scratch_mu;
+std::map<int, void*> g_scratch_dev;   // device -> device address of its `scratch`
+
+dsi_status scratch_address(int dev, void** out) {
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  auto it = g_scratch_dev.find(dev);
+  if (it != g_scratch_dev.end()) {
+    *out = it->second;
+    return DSI_OK;
+  }
+  void* p = nullptr;
+  const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+  if (e != hipSuccess || !p) {
+    hipGetLastError();
+    return fail(DSI_EHIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev, hipGetErrorString(e));
+  }
+  g_scratch_dev[dev] = p;
+  *out = p;
+  return DSI_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -1061,6 +1091,47 @@ dsi_status dsi_accept(void* stream, int32_t B, int32_t k, int32_t V, const float
   va.err = w.err;
   verify_bind_workspace(va, w.ws.p, B * (k + 1), B, V);
   HIP_TRY(launch_verify(va, (hipStream_t)stream));
+  return DSI_OK;
+}
+
+dsi_status dsi_accept_noalloc(void* stream, int32_t B, int32_t k, int32_t V, const float* d_logits,
+                              const int32_t* d_tokens, const float* d_q, const float* d_u,
+                              float temperature, int32_t mode, int32_t* d_n_accepted,
+                              int32_t* d_next_token) {
+  DSI_TRY(verify_args_ok(B, k, V, d_tokens, d_q, d_u, temperature, mode, d_n_accepted, d_next_token));
+  if (!d_logits) return fail(DSI_EINVAL, "null logits");
+  const size_t need = verify_workspace_bytes(B * (k + 1), B, V);
+  if (need > DSI_ACCEPT_NOALLOC_BYTES - kScratchHead)
+    return fail(DSI_ECAPACITY,
+                "dsi_accept_noalloc: %d rows over a vocabulary of %d need %zu workspace bytes; the "
+                "fixed array holds %zu",
+                B * (k + 1), V, need, (size_t)DSI_ACCEPT_NOALLOC_BYTES - kScratchHead);
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  void* base = nullptr;
+  DSI_TRY(scratch_address(dev, &base));
+  hipStream_t s = (hipStream_t)stream;
+  // the error word accumulates with atomics: clear it (a fill kernel, so the
+  // call stays capturable)
+  HIP_TRY(launch_fill_zero(base, sizeof(int), s));
+  VerifyArgs va{};
+  va.B = B;
+  va.k = k;
+  va.V = V;
+  va.logits = d_logits;
+  va.tokens = d_tokens;
+  va.q = d_q;
+  va.u = d_u;
+  va.temperature = (double)temperature;
+  va.greedy = mode == DSI_GREEDY;
+  va.commit = 0;
+  va.lens = nullptr;
+  va.window0 = 0;
+  va.n_out = d_n_accepted;
+  va.tok_out = d_next_token;
+  va.err = (int*)base;
+  verify_bind_workspace(va, (char*)base + kScratchHead, B * (k + 1), B, V);
+  HIP_TRY(launch_verify(va, s));
   return DSI_OK;
 }
 

@@ -26,6 +26,7 @@ TENSOR_IDS = {
 EXPORTED = (
     "dsi_model_create", "dsi_model_set_tensor", "dsi_model_destroy", "dsi_kv_create",
     "dsi_kv_destroy", "dsi_prefill", "dsi_verify", "dsi_verify_tree", "dsi_draft", "dsi_accept",
+    "dsi_accept_noalloc",
     "dsi_kv_rollback", "dsi_kv_length", "dsi_sync", "dsi_kv_export", "dsi_kv_import", "dsi_kv_set_length",
     "dsi_profile_begin", "dsi_profile_end", "dsi_profile_kernel", "dsi_last_error",
 )
@@ -88,6 +89,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "dsi_verify_tree": ([P, P, ctypes.POINTER(dsi_tree_args), P, P, P], I32),
         "dsi_draft": ([P, P, I32, P, I32, I32, P, F, P, P], I32),
         "dsi_accept": ([P, I32, I32, I32, P, P, P, P, F, I32, P, P], I32),
+        "dsi_accept_noalloc": ([P, I32, I32, I32, P, P, P, P, F, I32, P, P], I32),
         "dsi_kv_rollback": ([P, I32, I32], I32),
         "dsi_kv_length": ([P, I32, ctypes.POINTER(ctypes.c_int32)], I32),
         "dsi_sync": ([P], I32),
@@ -182,6 +184,13 @@ def dsi_accept(stream: int, n_windows: int, k: int, vocab: int, d_logits, d_toke
     _check(load().dsi_accept(stream or None, n_windows, k, vocab, _ptr(d_logits), _ptr(d_tokens),
                              _ptr(d_q), _ptr(d_u), temperature, mode, _ptr(d_n_accepted),
                              _ptr(d_next_token)))
+
+
+def dsi_accept_noalloc(stream: int, n_windows: int, k: int, vocab: int, d_logits, d_tokens, d_q, d_u,
+                       d_n_accepted, d_next_token, temperature: float = 1.0, mode: int = DSI_SAMPLE):
+    _check(load().dsi_accept_noalloc(stream or None, n_windows, k, vocab, _ptr(d_logits), _ptr(d_tokens),
+                                     _ptr(d_q), _ptr(d_u), temperature, mode, _ptr(d_n_accepted),
+                                     _ptr(d_next_token)))
 
 
 def dsi_kv_rollback(kv: int, window: int, new_len: int):

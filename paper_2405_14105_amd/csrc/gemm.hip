@@ -651,6 +651,211 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_f32(GemmArgs a) {
   if constexpr (EPI == EPI_PARTRES) part_fold<W_F32, NW>(a, nb0, nbv, fpre);
 }
 
+// ------------------------------------------------------------------ ring GEMM
+//
+// One-row-tile launches (M <= 16) over weights in the ring layout (RingCfg):
+// each of the 8 waves of a workgroup streams its own contiguous run of
+// nk * nbw tiles through a register ring of kRingDepth tiles.  The whole run
+// is unrolled at compile time, so the position of every load in the wave's
+// load order is static: consuming tile u waits for exactly the loads issued
+// before it while the next kRingDepth - 1 tiles stay in flight, and the ring
+// never drains until the wave's last tiles.  The activation fragments of a
+// k-block (hi and lo halves, token rows past M skipped by out-of-range buffer
+// loads) are requested just before its first weight tile, so they arrive
+// with it and their bytes are spread over the stream; the epilogue inputs
+// and RMSNorm sums are requested before everything else.  Partial tiles are
+// reduced across the waves through LDS in wave order and handed to the same
+// epilogues as the packed kernel.
+constexpr int kRingDepth = 8;
+
+// RMSNorm sums of rows w and w + kRingWaves (every row of a 16-row tile),
+// requested before the weights and reduced after the main loop
+struct RingSsq {
+  float v[2][kSsqPer];
+};
+template <int EPI>
+__device__ __forceinline__ RingSsq ring_ssq_prefetch(const GemmArgs& a) {
+  RingSsq r;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int c = 0; c < kSsqPer; ++c) r.v[h][c] = 0.f;
+  if constexpr (EPI == EPI_QKV || EPI == EPI_SILU) {
+    if (a.ssq) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int m = w + h * kRingWaves;
+        if (m < a.M) {
+          const float* p = a.ssq + (size_t)m * a.ssq_n;
+#pragma unroll
+          for (int c = 0; c < kSsqPer; ++c)
+            if (lane + 64 * c < a.ssq_n) r.v[h][c] = p[lane + 64 * c];
+        }
+      }
+    }
+  }
+  return r;
+}
+
+__device__ __forceinline__ void ring_row_scales(const GemmArgs& a, const RingSsq& pre, float* rs) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int m = w + h * kRingWaves;
+    float sum = 0.f;
+#pragma unroll
+    for (int c = 0; c < kSsqPer; ++c) sum += pre.v[h][c];
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) sum += __shfl_xor(sum, off);
+    if (lane == 0 && m < a.M) rs[m] = 1.0f / sqrtf(sum / (float)a.norm_d + a.eps);
+  }
+}
+
+template <int NK, int NBW, int EPI>
+__global__ __launch_bounds__(kRingWaves * 64) void k_gemm_ring(GemmArgs a) {
+  constexpr int NW = kRingWaves, D = kRingDepth, N = NK * NBW;
+  // activation slots: k-block i's fragments are requested together with its
+  // first weight tile (D tiles ahead of use) and live until its last tile
+  constexpr int A = (D + NBW - 1) / NBW + 1;
+  static_assert(N >= D, "a wave's run must fill the ring");
+  __shared__ f32x4 red[NW * NBW * 64];
+  __shared__ float rs[16];
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int g = blockIdx.x / a.S, split = blockIdx.x - g * a.S;
+  const int nb0 = g * NBW;
+  const int nbv = min(NBW, a.Nb - nb0);
+  const int kb0 = split * (NW * NK) + w * NK;
+  const u32x4* __restrict__ Ws = (const u32x4*)a.Ws + ((size_t)(blockIdx.x * NW + w) * N) * 64 + lane;
+  // activation packs as buffers: a lane whose token row is padding (>= M)
+  // or whose k-block lies past the matrix reads out of range, which returns
+  // zeros without a memory access
+  const int nrec = a.Kb * 1024;
+  const __amdgpu_buffer_rsrc_t Rh = __builtin_amdgcn_make_buffer_rsrc((void*)a.Xhi, (short)0, nrec, 0x00020000);
+  const __amdgpu_buffer_rsrc_t Rl = __builtin_amdgcn_make_buffer_rsrc((void*)a.Xlo, (short)0, nrec, 0x00020000);
+  const bool row_ok = (lane & 15) < a.M;
+  auto xoff = [&](int i) -> int {
+    return (row_ok && kb0 + i < a.Kb) ? ((kb0 + i) * 64 + lane) * 16 : 0x7ffffff0;
+  };
+
+  const EpiIn pre = epi_prefetch<1, NBW, NW, EPI>(a, nb0);
+  FoldIn fpre{};
+  if constexpr (EPI == EPI_PARTRES) fpre = fold_prefetch<1, NBW, NW>(a, nb0, nbv);
+  const RingSsq spre = ring_ssq_prefetch<EPI>(a);
+  __builtin_amdgcn_sched_barrier(0);
+  u32x4 ring[D];
+  u32x4 xh[A], xl[A];
+  // issue position u: the fragments of k-block u / NBW when u starts one,
+  // then weight tile u
+  auto issue = [&](int u) {
+    if (u % NBW == 0) {
+      const int i = u / NBW;
+      xh[i % A] = __builtin_amdgcn_raw_buffer_load_b128(Rh, xoff(i), 0, 0);
+      xl[i % A] = __builtin_amdgcn_raw_buffer_load_b128(Rl, xoff(i), 0, 0);
+    }
+    ring[u % D] = __builtin_nontemporal_load(Ws + (size_t)u * 64);
+  };
+#pragma unroll
+  for (int r = 0; r < D; ++r) {
+    issue(r);
+    __builtin_amdgcn_sched_barrier(0);   // issue order = ring order
+  }
+  f32x4 acc[NBW];
+#pragma unroll
+  for (int j = 0; j < NBW; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int u = 0; u < N; ++u) {
+    const bf16x8 wv = as_bf16x8(ring[u % D]);
+    const int i = u / NBW;
+    acc[u % NBW] = mfma_bf16(wv, as_bf16x8(xh[i % A]), acc[u % NBW]);
+    acc[u % NBW] = mfma_bf16(wv, as_bf16x8(xl[i % A]), acc[u % NBW]);
+    if (u + D < N) issue(u + D);
+    __builtin_amdgcn_sched_barrier(0);   // consume tile u, then refill its slot
+  }
+  if (a.ssq) ring_row_scales(a, spre, rs);
+#pragma unroll
+  for (int j = 0; j < NBW; ++j) red[(w * NBW + j) * 64 + lane] = acc[j];
+  __syncthreads();
+  finish<W_BF16, EPI, 1, NBW, NW>(a, red, a.ssq ? rs : nullptr, nb0, NBW, split, pre);
+  if constexpr (EPI == EPI_PARTRES) part_fold<W_BF16, NW>(a, nb0, nbv, fpre);
+}
+
+// n-blocks per workgroup of each role's ring layout: the O projection one
+// (256 workgroups at d = 4096), QKV two (192 at the 8B shape), gate/up
+// seven (one workgroup per CU for 1792 n-blocks), the down projection four
+// with its K split (as the packed launch)
+template <int EPI>
+struct RingRole;
+template <>
+struct RingRole<EPI_QKV> {
+  static constexpr int NBW = 2;
+};
+template <>
+struct RingRole<EPI_RESID> {
+  static constexpr int NBW = 1;
+};
+template <>
+struct RingRole<EPI_SILU> {
+  static constexpr int NBW = 7;
+};
+template <>
+struct RingRole<EPI_PART> {
+  static constexpr int NBW = 4;
+};
+template <>
+struct RingRole<EPI_PARTRES> : RingRole<EPI_PART> {};
+
+// k-blocks per wave the ring kernel is built for (a shape's k-range per wave
+// is rounded up to one of them; the extra tiles are zero)
+constexpr int kRingNk[] = {1, 2, 4, 8, 14, 16};
+
+template <int EPI, int NK>
+hipError_t launch_ring_nk(const GemmArgs& a, hipStream_t s) {
+  constexpr int NBW = RingRole<EPI>::NBW;
+  if constexpr (NK * NBW < kRingDepth) {
+    return hipErrorInvalidValue;
+  } else {
+    const int grid = ((a.Nb + NBW - 1) / NBW) * a.S;
+    hipLaunchKernelGGL((k_gemm_ring<NK, NBW, EPI>), dim3(grid), dim3(kRingWaves * 64), 0, s, a);
+    return hipGetLastError();
+  }
+}
+
+template <int EPI>
+hipError_t launch_ring(const GemmArgs& a, hipStream_t s) {
+  switch (a.ring_nk) {
+    case 1: return launch_ring_nk<EPI, 1>(a, s);
+    case 2: return launch_ring_nk<EPI, 2>(a, s);
+    case 4: return launch_ring_nk<EPI, 4>(a, s);
+    case 8: return launch_ring_nk<EPI, 8>(a, s);
+    case 14: return launch_ring_nk<EPI, 14>(a, s);
+    case 16: return launch_ring_nk<EPI, 16>(a, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+// ring layout from the packed layout: one thread per 16 bytes of a tile
+__global__ void k_restream(const u32x4* __restrict__ src, int Nb, int Kb, int G, RingCfg c,
+                           u32x4* __restrict__ dst) {
+  const size_t total = c.tiles() * 64;
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < total;
+       i += (size_t)gridDim.x * blockDim.x) {
+    const int lane = (int)(i & 63);
+    const size_t t = i >> 6;
+    const int run = c.nk * c.nbw;                       // tiles per wave
+    const size_t wave = t / run;                        // blockIdx * waves + w
+    const int u = (int)(t - wave * run);
+    const int wg = (int)(wave / kRingWaves), w = (int)(wave % kRingWaves);
+    const int ii = u / c.nbw, j = u % c.nbw;
+    const int nb = (wg / c.S) * c.nbw + j;
+    const int kb = (wg % c.S) * (kRingWaves * c.nk) + w * c.nk + ii;
+    u32x4 v{0u, 0u, 0u, 0u};
+    if (nb < Nb && kb < Kb) v = src[wtile_index(nb, kb, Nb, Kb, G) * 64 + lane];
+    dst[i] = v;
+  }
+}
+
 // Grid shaping.  Each wave reuses every activation fragment it loads across
 // the NBW n-blocks of its workgroup (activation reads from L2, not the
 // weight stream, are what limit a one-n-block-per-wave GEMM); waves split K
@@ -777,8 +982,55 @@ int gemm_wgroup(int wtype, int epi_kind, int Nb) {
   return 1;
 }
 
+bool ring_config(int wtype, int epi_kind, int Nb, int Kb, int S, RingCfg* out) {
+  *out = RingCfg{};
+  if (wtype != W_BF16 || Nb < 1 || Kb < 1 || S < 1) return false;
+  int nbw = 0;
+  switch (epi_kind) {
+    case EPI_QKV: nbw = RingRole<EPI_QKV>::NBW; break;
+    case EPI_RESID: nbw = RingRole<EPI_RESID>::NBW; break;
+    case EPI_SILU: nbw = RingRole<EPI_SILU>::NBW; break;
+    case EPI_PART:
+    case EPI_PARTRES: nbw = RingRole<EPI_PART>::NBW; break;
+    default: return false;
+  }
+  if (S > 1 && epi_kind != EPI_PART && epi_kind != EPI_PARTRES) return false;
+  const int need = (Kb + S * kRingWaves - 1) / (S * kRingWaves);   // k-blocks per wave
+  int nk = 0;
+  for (int v : kRingNk)
+    if (v >= need && v * nbw >= kRingDepth) {
+      nk = v;
+      break;
+    }
+  if (!nk) return false;
+  out->nbw = nbw;
+  out->nk = nk;
+  out->S = S;
+  out->wgs = ((Nb + nbw - 1) / nbw) * S;
+  return true;
+}
+
+hipError_t launch_restream(const void* src, int Nb, int Kb, int G, const RingCfg& c, void* dst,
+                           hipStream_t s) {
+  if (c.nbw < 1 || c.nk < 1 || c.S < 1 || G < 1) return hipErrorInvalidValue;
+  const size_t total = c.tiles() * 64;
+  const int grid = (int)std::min<size_t>((total + 255) / 256, 65536);
+  hipLaunchKernelGGL(k_restream, dim3(grid), dim3(256), 0, s, (const u32x4*)src, Nb, Kb, G, c, (u32x4*)dst);
+  return hipGetLastError();
+}
+
 hipError_t launch_gemm(int wtype, int mt, const GemmArgs& a, hipStream_t s) {
   if (a.Nb <= 0 || a.M <= 0) return hipSuccess;
+  if (a.Ws && mt == 1 && wtype == W_BF16 && a.M <= 16) {
+    switch (a.epi.kind) {
+      case EPI_QKV: return launch_ring<EPI_QKV>(a, s);
+      case EPI_RESID: return launch_ring<EPI_RESID>(a, s);
+      case EPI_SILU: return launch_ring<EPI_SILU>(a, s);
+      case EPI_PART: return launch_ring<EPI_PART>(a, s);
+      case EPI_PARTRES: return launch_ring<EPI_PARTRES>(a, s);
+    }
+    return hipErrorInvalidValue;
+  }
   if (a.G < 1 || (wtype != W_BF16 && a.G != 1)) return hipErrorInvalidValue;
   if (a.S < 1 || (a.S > 1 && a.epi.kind != EPI_PART && a.epi.kind != EPI_PARTRES)) return hipErrorInvalidValue;
   switch (a.epi.kind) {

@@ -107,6 +107,10 @@ struct EpiArgs {
 
 struct GemmArgs {
   const void* W;
+  // Nullable: the same weights in the ring (stream) layout of the role's
+  // RingCfg; one-row-tile launches that set it run the ring kernel.
+  const void* Ws = nullptr;
+  int ring_nk = 0;      // k-blocks per wave of that layout
   const void* Xhi;
   const void* Xlo;
   int Nb, Kb, M;
@@ -135,6 +139,29 @@ __host__ __device__ inline size_t wtile_index(int nb, int kb, int Nb, int Kb, in
 // workgroup of its one-row-tile launch (bf16 gate/up and LM head), else 1.
 int gemm_wgroup(int wtype, int epi_kind, int Nb);
 constexpr int kMaxSplits = 4;
+
+// Ring layout of a GEMM weight for one-row-tile launches (gemm.hip,
+// k_gemm_ring).  A launch has `wgs` workgroups of kRingWaves waves; workgroup
+// g*S + s owns n-blocks [g*nbw, g*nbw + nbw) and the K split s, i.e. k-blocks
+// [s*kRingWaves*nk, (s+1)*kRingWaves*nk), of which wave w takes the nk
+// consecutive ones starting at s*kRingWaves*nk + w*nk.  Every wave's tiles
+// are one contiguous run in the order it consumes them, k-block major:
+//   tile (wave, i, j) = ((wg * kRingWaves + w) * nk + i) * nbw + j
+// (1 KB each); tiles past the matrix (n-block >= Nb or k-block >= Kb) are 0.
+constexpr int kRingWaves = 8;
+struct RingCfg {
+  int nbw = 0;          // n-blocks per workgroup (0: no ring layout for this role)
+  int nk = 0;           // k-blocks per wave
+  int S = 1;            // K splits across workgroups
+  int wgs = 0;          // workgroups of a launch
+  __host__ __device__ size_t tiles() const { return (size_t)wgs * kRingWaves * nk * nbw; }
+};
+// Ring layout of a role's weight (epi_kind) of Nb x Kb tiles split S ways
+// along K; false when the role has none (the launch uses the packed layout).
+bool ring_config(int wtype, int epi_kind, int Nb, int Kb, int S, RingCfg* out);
+// src: the packed layout (wtile_index with group G) -> dst: ring layout
+hipError_t launch_restream(const void* src, int Nb, int Kb, int G, const RingCfg& c, void* dst,
+                           hipStream_t s);
 
 // launchers (gemm.hip)
 hipError_t launch_gemm(int wtype, int mt, const GemmArgs& a, hipStream_t s);

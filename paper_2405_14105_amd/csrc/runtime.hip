@@ -82,6 +82,11 @@ struct LayerW {
   void* wo = nullptr;
   void* wgu = nullptr;
   void* wdown = nullptr;
+  // the same matrices in the ring layout of their role (nullable)
+  void* wqkv_s = nullptr;
+  void* wo_s = nullptr;
+  void* wgu_s = nullptr;
+  void* wdown_s = nullptr;
 };
 
 struct dsi_model {
@@ -92,6 +97,10 @@ struct dsi_model {
   int Kb_d = 0, Kb_q = 0, Kb_ff = 0;
   int Nb_qkv = 0, Nb_o = 0, Nb_gu = 0, Nb_down = 0, Nb_head = 0;
   int G_gu = 1, G_head = 1;   // n-block groups of the packed gate/up and LM head
+  // ring layouts of the four layer GEMMs (nbw == 0: the role has none) and
+  // whether one-row-tile forwards on single-window caches use them
+  RingCfg rc_qkv, rc_o, rc_gu, rc_down;
+  bool use_ring = true;
   void* embed = nullptr;
   float* final_norm = nullptr;
   void* lm_head = nullptr;
@@ -224,11 +233,21 @@ struct Prof {
 //           after the last layer the final RMSNorm folds them
 //   QKV     (layers >= 1) scaled by the RMSNorm of x from ssq2
 //   head    final-normed pack pk_d -> logits
-GemmArgs qkv_args(dsi_model* m, dsi_kv* kv, int l, int M, RowMap rows) {
+// Ring layout of one role for a launch (a one-row-tile forward on a
+// single-window cache): see ring_forward.
+void set_ring(GemmArgs& g, const RingCfg& c, const void* ws, bool ring) {
+  if (ring && c.nbw && ws) {
+    g.Ws = ws;
+    g.ring_nk = c.nk;
+  }
+}
+
+GemmArgs qkv_args(dsi_model* m, dsi_kv* kv, int l, int M, RowMap rows, bool ring = false) {
   GemmArgs g{};
   g.M = M;
   g.S = 1;
   g.W = m->layers[l].wqkv;
+  set_ring(g, m->rc_qkv, m->layers[l].wqkv_s, ring);
   g.Xhi = m->pk_d.hi;
   g.Xlo = m->pk_d.lo;
   g.Nb = m->Nb_qkv;
@@ -253,11 +272,12 @@ GemmArgs qkv_args(dsi_model* m, dsi_kv* kv, int l, int M, RowMap rows) {
   return g;
 }
 
-GemmArgs oproj_args(dsi_model* m, int l, int M) {
+GemmArgs oproj_args(dsi_model* m, int l, int M, bool ring = false) {
   GemmArgs g{};
   g.M = M;
   g.S = 1;
   g.W = m->layers[l].wo;
+  set_ring(g, m->rc_o, m->layers[l].wo_s, ring);
   g.Xhi = m->pk_q.hi;
   g.Xlo = m->pk_q.lo;
   g.Nb = m->Nb_o;
@@ -272,11 +292,12 @@ GemmArgs oproj_args(dsi_model* m, int l, int M) {
   return g;
 }
 
-GemmArgs gateup_args(dsi_model* m, int l, int M) {
+GemmArgs gateup_args(dsi_model* m, int l, int M, bool ring = false) {
   GemmArgs g{};
   g.M = M;
   g.S = 1;
   g.W = m->layers[l].wgu;
+  set_ring(g, m->rc_gu, m->layers[l].wgu_s, ring);
   g.Xhi = m->pk_d.hi;
   g.Xlo = m->pk_d.lo;
   g.Nb = m->Nb_gu;
@@ -292,15 +313,20 @@ GemmArgs gateup_args(dsi_model* m, int l, int M) {
   return g;
 }
 
-GemmArgs down_args(dsi_model* m, int l, int M, int mt, float* hidden_next = nullptr) {
+GemmArgs down_args(dsi_model* m, int l, int M, int mt, float* hidden_next = nullptr, bool ring = false) {
   GemmArgs g{};
   g.M = M;
   g.W = m->layers[l].wdown;
+  set_ring(g, m->rc_down, m->layers[l].wdown_s, ring);
   g.Xhi = m->pk_ff.hi;
   g.Xlo = m->pk_ff.lo;
   g.Nb = m->Nb_down;
   g.Kb = m->Kb_ff;
   g.S = gemm_part_splits(m->wtype, m->Nb_down, m->Kb_ff, mt);
+  if (g.Ws && g.S != m->rc_down.S) {   // the ring layout was built for another split
+    g.Ws = nullptr;
+    g.ring_nk = 0;
+  }
   g.epi.kind = EPI_PART;
   g.epi.out = m->delta;
   g.epi.ld = m->d;
@@ -382,6 +408,14 @@ dsi_status plan_attention(dsi_model* m, dsi_kv* kv, int window0, int B, int R, A
   return DSI_OK;
 }
 
+// Whether a forward runs its layer GEMMs on the ring layouts: one row tile
+// (at most 16 rows) on a cache of one window.  A cache of several windows
+// (verification tasks batched together) always takes the packed kernels, so
+// a window gives bit-identical results alone or inside a batch of its cache.
+bool ring_forward(const dsi_model* m, const dsi_kv* kv, int mt) {
+  return m->use_ring && m->wtype == W_BF16 && mt == 1 && kv->n_windows == 1;
+}
+
 // Stream-ordered launches only (capturable into a graph).  depth / anc
 // (nullable, device [M]): token-tree rows (RowMap::depth, AttnArgs::anc).
 dsi_status run_forward(dsi_model* m, dsi_kv* kv, const AttnPlan& ap, int window0, int B, int R,
@@ -392,6 +426,7 @@ dsi_status run_forward(dsi_model* m, dsi_kv* kv, const AttnPlan& ap, int window0
   const int mt = cdiv(M, 16);
   RowMap rows{kv->lens, window0, R, depth};
   const size_t Md = (size_t)M * m->d;
+  const bool ring = ring_forward(m, kv, mt);
 
   EmbedArgs ea{};
   ea.tokens = d_tokens;
@@ -418,7 +453,7 @@ dsi_status run_forward(dsi_model* m, dsi_kv* kv, const AttnPlan& ap, int window0
     // fused QKV + RoPE + KV append
     {
       Prof p(m, DSI_K_QKV);
-      HIP_TRY(launch_gemm(m->wtype, mt, qkv_args(m, kv, l, M, rows), s));
+      HIP_TRY(launch_gemm(m->wtype, mt, qkv_args(m, kv, l, M, rows, ring), s));
     }
 
     AttnArgs aa{};
@@ -448,17 +483,17 @@ dsi_status run_forward(dsi_model* m, dsi_kv* kv, const AttnPlan& ap, int window0
     // O projection: residual update in place, FFN-norm input for gate/up
     {
       Prof p(m, DSI_K_OPROJ);
-      HIP_TRY(launch_gemm(m->wtype, mt, oproj_args(m, l, M), s));
+      HIP_TRY(launch_gemm(m->wtype, mt, oproj_args(m, l, M, ring), s));
     }
     // gate/up (RMSNorm scale applied to the accumulators) + SwiGLU
     {
       Prof p(m, DSI_K_GATEUP);
-      HIP_TRY(launch_gemm(m->wtype, mt, gateup_args(m, l, M), s));
+      HIP_TRY(launch_gemm(m->wtype, mt, gateup_args(m, l, M, ring), s));
     }
     // down projection into K-split partials
     // down projection; below the last layer it also folds the residual and
     // prepares the next layer's normed input (EPI_PARTRES)
-    const GemmArgs gd = down_args(m, l, M, mt, hidden ? hidden + (size_t)(l + 1) * Md : nullptr);
+    const GemmArgs gd = down_args(m, l, M, mt, hidden ? hidden + (size_t)(l + 1) * Md : nullptr, ring);
     {
       Prof p(m, DSI_K_DOWN);
       HIP_TRY(launch_gemm(m->wtype, mt, gd, s));
@@ -651,6 +686,13 @@ dsi_status dsi_model_create(const dsi_config* cfg, void* stream, dsi_model** out
   m->Nb_head = cdiv(m->V, 16);
   m->G_gu = gemm_wgroup(m->wtype, EPI_SILU, m->Nb_gu);
   m->G_head = gemm_wgroup(m->wtype, EPI_STORE, m->Nb_head);
+  const char* rg = getenv("DSI_RING");
+  m->use_ring = !(rg && rg[0] == '0');
+  ring_config(m->wtype, EPI_QKV, m->Nb_qkv, m->Kb_d, 1, &m->rc_qkv);
+  ring_config(m->wtype, EPI_RESID, m->Nb_o, m->Kb_q, 1, &m->rc_o);
+  ring_config(m->wtype, EPI_SILU, m->Nb_gu, m->Kb_d, 1, &m->rc_gu);
+  ring_config(m->wtype, EPI_PARTRES, m->Nb_down, m->Kb_ff,
+              gemm_part_splits(m->wtype, m->Nb_down, m->Kb_ff, 1), &m->rc_down);
   m->layers.resize(m->L);
   m->set_mask.assign(m->L + 1, 0u);
 
@@ -670,6 +712,12 @@ dsi_status dsi_model_create(const dsi_config* cfg, void* stream, dsi_model** out
     A(&w.wo, (size_t)m->Nb_o * m->Kb_q * tile * m->esz);
     A(&w.wgu, (size_t)m->Nb_gu * m->Kb_d * tile * m->esz);
     A(&w.wdown, (size_t)m->Nb_down * m->Kb_ff * tile * m->esz);
+    if (m->use_ring) {
+      if (m->rc_qkv.nbw) A(&w.wqkv_s, m->rc_qkv.tiles() * tile * m->esz);
+      if (m->rc_o.nbw) A(&w.wo_s, m->rc_o.tiles() * tile * m->esz);
+      if (m->rc_gu.nbw) A(&w.wgu_s, m->rc_gu.tiles() * tile * m->esz);
+      if (m->rc_down.nbw) A(&w.wdown_s, m->rc_down.tiles() * tile * m->esz);
+    }
   }
   A((void**)&m->x, (size_t)kMaxRows * m->d * 4);
   A((void**)&m->delta, (size_t)kMaxSplits * kMaxRows * m->d * 4);
@@ -805,6 +853,25 @@ dsi_status dsi_model_set_tensor(dsi_model* m, int32_t layer, int32_t id, const v
     if (e != hipSuccess) return fail(DSI_EHIP, "prepack: %s", hipGetErrorString(e));
   }
   m->set_mask[global ? 0 : layer + 1] |= 1u << id;
+  if (!global) {
+    // once every part of a role's matrix is packed, lay it out for the ring
+    // kernel as well
+    const unsigned have = m->set_mask[layer + 1];
+    LayerW& lw = m->layers[layer];
+    hipError_t e = hipSuccess;
+    const unsigned qkv = (1u << DSI_T_WQ) | (1u << DSI_T_WK) | (1u << DSI_T_WV);
+    const unsigned gu = (1u << DSI_T_W_GATE) | (1u << DSI_T_W_UP);
+    if ((id == DSI_T_WQ || id == DSI_T_WK || id == DSI_T_WV) && (have & qkv) == qkv && lw.wqkv_s)
+      e = launch_restream(lw.wqkv, m->Nb_qkv, m->Kb_d, 1, m->rc_qkv, lw.wqkv_s, nullptr);
+    else if (id == DSI_T_WO && lw.wo_s)
+      e = launch_restream(lw.wo, m->Nb_o, m->Kb_q, 1, m->rc_o, lw.wo_s, nullptr);
+    else if ((id == DSI_T_W_GATE || id == DSI_T_W_UP) && (have & gu) == gu && lw.wgu_s)
+      e = launch_restream(lw.wgu, m->Nb_gu, m->Kb_d, m->G_gu, m->rc_gu, lw.wgu_s, nullptr);
+    else if (id == DSI_T_W_DOWN && lw.wdown_s)
+      e = launch_restream(lw.wdown, m->Nb_down, m->Kb_ff, 1, m->rc_down, lw.wdown_s, nullptr);
+    if (e == hipSuccess) e = hipDeviceSynchronize();
+    if (e != hipSuccess) return fail(DSI_EHIP, "ring layout: %s", hipGetErrorString(e));
+  }
   return DSI_OK;
 }
 
@@ -1094,6 +1161,7 @@ dsi_status dsi_accept(void* stream, int32_t B, int32_t k, int32_t V, const float
   return DSI_OK;
 }
 
+
 dsi_status dsi_accept_noalloc(void* stream, int32_t B, int32_t k, int32_t V, const float* d_logits,
                               const int32_t* d_tokens, const float* d_q, const float* d_u,
                               float temperature, int32_t mode, int32_t* d_n_accepted,
@@ -1194,13 +1262,14 @@ dsi_status dsi_profile_kernel(dsi_model* m, dsi_kv* kv, int32_t cls, int32_t rou
   const size_t dstride = (size_t)kMaxRows * m->d;
   hipStream_t s = m->stream;
   const RowMap rows{kv->lens, m->last_window0, m->last_R};
+  const bool ring = ring_forward(m, kv, mt);
   auto one = [&](int l) -> dsi_status {
     GemmArgs g;
     switch (cls) {
-      case DSI_K_QKV: g = qkv_args(m, kv, l, M, rows); break;
-      case DSI_K_OPROJ: g = oproj_args(m, l, M); break;
-      case DSI_K_GATEUP: g = gateup_args(m, l, M); break;
-      case DSI_K_DOWN: g = down_args(m, l, M, mt); break;
+      case DSI_K_QKV: g = qkv_args(m, kv, l, M, rows, ring); break;
+      case DSI_K_OPROJ: g = oproj_args(m, l, M, ring); break;
+      case DSI_K_GATEUP: g = gateup_args(m, l, M, ring); break;
+      case DSI_K_DOWN: g = down_args(m, l, M, mt, nullptr, ring); break;
       default: g = head_args(m, m->logits, M); break;
     }
     HIP_TRY(launch_gemm(m->wtype, mt, g, s));

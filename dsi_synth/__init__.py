@@ -99,6 +99,12 @@ SHAPES = {
     # many KV heads and query tiles: few key chunks per (window, KV head),
     # so waves take several 32-key steps once the cache is a few thousand long
     "many_kv": Shape("many_kv", 2, 256, 64, 16, 32, 400, 1500, gains="random"),
+    # the 1B / 8B attention geometry (32 query heads over 8 KV heads, head
+    # dim 64 / 128) on a small residual stream: the O projection takes its
+    # ring layout (one n-block per workgroup, 8 / 16 k-blocks per wave), as
+    # at the full shapes
+    "o_ring_hd64": Shape("o_ring_hd64", 2, 256, 32, 8, 64, 688, 2050, gains="random"),
+    "o_ring_hd128": Shape("o_ring_hd128", 2, 256, 32, 8, 128, 344, 1003, gains="random"),
     # drafters: small models sharing a target's vocabulary
     "tiny_draft": Shape("tiny_draft", 1, 64, 2, 2, 32, 128, 1024, wdtype="f32", kvdtype="f32"),
     "ragged_draft": Shape("ragged_draft", 1, 96, 3, 1, 32, 200, 1003, gains="random"),

@@ -263,6 +263,15 @@ dsi_status dsi_accept_noalloc(void* stream, int32_t n_windows, int32_t k, int32_
  * call returns DSI_EINVAL). */
 dsi_status dsi_kv_rollback(dsi_kv* kv, int32_t window, int32_t new_len);
 
+/* Fill the dead rows of one window -- positions [length, capacity) of K and
+ * V in every layer, the length being the device's when the fill runs -- with
+ * NaN.  Stream-ordered.  After a rollback this turns any read of a dead row
+ * (Section 3.1, "KV cache": rows of terminated threads) into NaN logits, so
+ * tests can show that no kernel lets such rows reach a result.  Rows are
+ * rewritten before they are read again by prefill and verification.
+ * Diagnostics and tests only. */
+dsi_status dsi_kv_poison(dsi_kv* kv, int32_t window);
+
 /* Current length of a window.  Synchronises the stream. */
 dsi_status dsi_kv_length(dsi_kv* kv, int32_t window, int32_t* len);
 

@@ -223,6 +223,33 @@ __global__ __launch_bounds__(NWV * 64, (NWV == 4 && KVB) ? 3 : 1) void k_attn(At
 #pragma unroll
     for (int t = 0; t < DT; ++t) o[t] *= alpha;
 
+    // keys at or past c1 (past the window's rows: dead cache rows or beyond
+    // the allocation) have probability 0, but 0 * NaN is not 0: their V
+    // elements are zeroed, so that whatever a dead row holds never reaches
+    // the output (dsi_kv_poison)
+    const int nv = c1 - (p0 + kgrp);   // valid keys among the lane's 8
+    if (nv < 8) {
+      if (KVB) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const uint32_t keep = (2 * i < nv ? 0x0000FFFFu : 0u) | (2 * i + 1 < nv ? 0xFFFF0000u : 0u);
+#pragma unroll
+          for (int t = 0; t < DT; ++t) d16.v[t][i] &= keep;
+        }
+      } else {
+        auto zero4 = [&](float4& x, int e0) {
+          x.x = e0 < nv ? x.x : 0.f;
+          x.y = e0 + 1 < nv ? x.y : 0.f;
+          x.z = e0 + 2 < nv ? x.z : 0.f;
+          x.w = e0 + 3 < nv ? x.w : 0.f;
+        };
+#pragma unroll
+        for (int t = 0; t < DT; ++t) {
+          zero4(d32.v[t].a, 0);
+          zero4(d32.v[t].b, 4);
+        }
+      }
+    }
     if (KVB) {
       bf16x8 ph, pl;
 #pragma unroll
@@ -259,16 +286,9 @@ __global__ __launch_bounds__(NWV * 64, (NWV == 4 && KVB) ? 3 : 1) void k_attn(At
   } else if constexpr (PIPE == 1) {
     for (int p0 = pfirst; p0 < c1; p0 += stride) step(p0, b16, b32, p0 + stride);
   } else if (pfirst < c1) {
-    // the first step runs on the loads issued above, outside the loop, so
-    // its S MFMAs wait for its K loads only (loads retire in order, and a
-    // loop header would merge in the later steps' loads); later steps issue
-    // every K and V load of the step before any math
+    // unpipelined plans have chunk == 32 * NWV (launch_main takes PIPE 0
+    // only then): a single step per wave, on the loads issued above
     step(pfirst, b16, b32, -1);
-    for (int p0 = pfirst + stride; p0 < c1; p0 += stride) {
-      load_k_into(b16, b32, p0);
-      load_v_into(b16, b32, p0);
-      step(p0, b16, b32, -1);
-    }
   }
 
   // combine the waves of this workgroup into one partial (m, l, O)

@@ -1,6 +1,8 @@
 // Elementwise passes: weight pre-packing, embedding gather + RMSNorm into a
 // GEMM activation pack (plus the rotary cos/sin table of the window
 // positions), RMSNorm into a pack, and KV length / content operations.
+#include <limits>
+
 #include "device_util.h"
 
 namespace dsi {
@@ -223,6 +225,24 @@ __global__ void k_kv_copy(int to_cache, T* kc, T* vc, int n_kv, int hd, int maxl
   }
 }
 
+// NaN into the dead rows [lens[window], maxlen) of one window: one block per
+// (layer, KV head); kc / vc: the window's layer-0 K and V, layer_stride
+// elements apart; V in the blocked layout [head][maxlen/32][hd][32]
+template <typename T>
+__global__ void k_kv_poison(T* kc, T* vc, size_t layer_stride, int n_kv, int hd, int maxlen, const int* lens,
+                            int window, T nan) {
+  const int layer = blockIdx.x / n_kv, h = blockIdx.x % n_kv;
+  const int len = lens[window];
+  T* k = kc + layer * layer_stride + (size_t)h * maxlen * hd;
+  T* v = vc + layer * layer_stride + (size_t)h * maxlen * hd;
+  const size_t n = (size_t)(maxlen - len) * hd;
+  for (size_t i = threadIdx.x; i < n; i += blockDim.x) {
+    const int p = len + (int)(i / hd), dd = (int)(i % hd);
+    k[(size_t)p * hd + dd] = nan;
+    v[((size_t)(p >> 5) * hd + dd) * 32 + (p & 31)] = nan;
+  }
+}
+
 __global__ void k_fill_zero(uint32_t* p, size_t n) {
   for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
     p[i] = 0u;
@@ -307,6 +327,18 @@ hipError_t launch_kv_copy(int to_cache, int kv_bf16, void* kc, void* vc, int n_k
   else
     hipLaunchKernelGGL(k_kv_copy<float>, dim3(g), dim3(256), 0, s, to_cache, (float*)kc, (float*)vc,
                        n_kv, hd, maxlen, len, (float*)dk, (float*)dv);
+  return hipGetLastError();
+}
+
+hipError_t launch_kv_poison(int kv_bf16, void* kc, void* vc, size_t layer_stride, int n_layers, int n_kv, int hd,
+                            int maxlen, const int* lens, int window, hipStream_t s) {
+  const dim3 grid(n_layers * n_kv), blk(256);
+  if (kv_bf16)
+    hipLaunchKernelGGL(k_kv_poison<uint16_t>, grid, blk, 0, s, (uint16_t*)kc, (uint16_t*)vc, layer_stride, n_kv,
+                       hd, maxlen, lens, window, (uint16_t)0x7FC0u);
+  else
+    hipLaunchKernelGGL(k_kv_poison<float>, grid, blk, 0, s, (float*)kc, (float*)vc, layer_stride, n_kv, hd,
+                       maxlen, lens, window, std::numeric_limits<float>::quiet_NaN());
   return hipGetLastError();
 }
 

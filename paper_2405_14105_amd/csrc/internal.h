@@ -305,6 +305,10 @@ hipError_t launch_kv_add_checked(int* lens, int window, const int* tokens, int n
 hipError_t launch_kv_copy(int to_cache, int kv_bf16, void* kc, void* vc, int n_kv, int hd,
                           int maxlen, int len, void* dk, void* dv, hipStream_t s);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
+// NaN into rows [lens[window], maxlen) of every layer's K and V of one window
+// (kc / vc: the window's layer-0 base; layers layer_stride elements apart)
+hipError_t launch_kv_poison(int kv_bf16, void* kc, void* vc, size_t layer_stride, int n_layers, int n_kv, int hd,
+                            int maxlen, const int* lens, int window, hipStream_t s);
 hipError_t launch_copy_rows(const float* src, float* dst, size_t n, hipStream_t s);
 
 }  // namespace dsi

@@ -1214,6 +1214,16 @@ dsi_status dsi_kv_rollback(dsi_kv* kv, int32_t window, int32_t new_len) {
   return DSI_OK;
 }
 
+dsi_status dsi_kv_poison(dsi_kv* kv, int32_t window) {
+  if (!kv) return fail(DSI_EINVAL, "null kv");
+  if (window < 0 || window >= kv->n_windows) return fail(DSI_EINVAL, "bad window %d", window);
+  dsi_model* m = kv->m;
+  HIP_TRY(launch_kv_poison(m->kvb, kv_ptr(kv, kv->k, 0, window), kv_ptr(kv, kv->v, 0, window),
+                           (size_t)kv->n_windows * kv->win_elems, m->L, m->hkv, m->hd, kv->maxlen_pad, kv->lens,
+                           window, m->stream));
+  return DSI_OK;
+}
+
 dsi_status dsi_kv_length(dsi_kv* kv, int32_t window, int32_t* len) {
   if (!kv || !len) return fail(DSI_EINVAL, "null argument");
   if (window < 0 || window >= kv->n_windows) return fail(DSI_EINVAL, "bad window %d", window);

@@ -27,7 +27,7 @@ EXPORTED = (
     "dsi_model_create", "dsi_model_set_tensor", "dsi_model_destroy", "dsi_kv_create",
     "dsi_kv_destroy", "dsi_prefill", "dsi_verify", "dsi_verify_tree", "dsi_draft", "dsi_accept",
     "dsi_accept_noalloc",
-    "dsi_kv_rollback", "dsi_kv_length", "dsi_sync", "dsi_kv_export", "dsi_kv_import", "dsi_kv_set_length",
+    "dsi_kv_rollback", "dsi_kv_poison", "dsi_kv_length", "dsi_sync", "dsi_kv_export", "dsi_kv_import", "dsi_kv_set_length",
     "dsi_profile_begin", "dsi_profile_end", "dsi_profile_kernel", "dsi_last_error",
 )
 DSI_K_QKV, DSI_K_ATTN, DSI_K_OPROJ, DSI_K_GATEUP, DSI_K_DOWN, DSI_K_HEAD, DSI_K_VERIFY = range(1, 8)
@@ -91,6 +91,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "dsi_accept": ([P, I32, I32, I32, P, P, P, P, F, I32, P, P], I32),
         "dsi_accept_noalloc": ([P, I32, I32, I32, P, P, P, P, F, I32, P, P], I32),
         "dsi_kv_rollback": ([P, I32, I32], I32),
+        "dsi_kv_poison": ([P, I32], I32),
         "dsi_kv_length": ([P, I32, ctypes.POINTER(ctypes.c_int32)], I32),
         "dsi_sync": ([P], I32),
         "dsi_kv_export": ([P, I32, I32, I32, P, P], I32),
@@ -195,6 +196,10 @@ def dsi_accept_noalloc(stream: int, n_windows: int, k: int, vocab: int, d_logits
 
 def dsi_kv_rollback(kv: int, window: int, new_len: int):
     _check(load().dsi_kv_rollback(kv, window, new_len))
+
+
+def dsi_kv_poison(kv: int, window: int):
+    _check(load().dsi_kv_poison(kv, window))
 
 
 def dsi_kv_length(kv: int, window: int) -> int:

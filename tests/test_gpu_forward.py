@@ -39,6 +39,10 @@ CASES = [
     ("mha_hd128", 70, 7),
     ("hd96_kvf32", 41, 5),
     ("f32w_bf16kv", 36, 4),
+    # the 1B / 8B attention geometry on a small residual stream: the O
+    # projection runs on its ring layout; 700 keys span three key chunks
+    ("o_ring_hd64", 700, 5),
+    ("o_ring_hd128", 300, 10),
 ]
 
 

@@ -57,6 +57,42 @@ def build(jobs: int = 0, verbose: bool = False) -> str:
     return LIB
 
 
+# Host-side sanitizer build: every source compiled with AddressSanitizer and
+# UndefinedBehaviorSanitizer on its host code (the C ABI, its validation and
+# the launchers) into a separate library.  The sanitizers apply to host code
+# only (-Xarch_host before each -fsanitize); the device code is built at -O1
+# (it is there for the kernel registration, not to be run).  The program that
+# loads the library must itself be linked with -fsanitize=address,undefined
+# (it provides the runtime).
+SAN_FLAGS = [f"--offload-arch={ARCH}", "-O1", "-g", "-fno-omit-frame-pointer", "-std=c++17", "-fPIC",
+             "-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+             "-I", os.path.join(ROOT, "include"), "-I", CSRC,
+             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+
+
+def build_host_sanitized(out_dir: str, jobs: int = 0) -> str:
+    """Build libdsi_san.so (host code only, ASan + UBSan) into out_dir."""
+    os.makedirs(out_dir, exist_ok=True)
+
+    def one(src):
+        obj = os.path.join(out_dir, os.path.splitext(src)[0] + ".san.o")
+        r = subprocess.run([HIPCC, *SAN_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj],
+                           capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"hipcc (sanitized host) failed for {src}:\n{r.stdout}\n{r.stderr}")
+        return obj
+
+    jobs = jobs or min(len(SOURCES), os.cpu_count() or 1)
+    with ThreadPoolExecutor(jobs) as ex:
+        objs = list(ex.map(one, SOURCES))
+    lib = os.path.join(out_dir, "libdsi_san.so")
+    r = subprocess.run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-Xarch_host", "-fsanitize=address",
+                        "-Xarch_host", "-fsanitize=undefined", "-o", lib, *objs], capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"link (sanitized host) failed:\n{r.stdout}\n{r.stderr}")
+    return lib
+
+
 if __name__ == "__main__":
     ap = argparse.ArgumentParser()
     ap.add_argument("--jobs", type=int, default=0)

@@ -571,14 +571,21 @@ def main():
     gb = gemm_bytes(wl.shape, M)
     gu_bytes = gb["gate_up"]
     achieved = gu_bytes / (gu["isolated_avg_ms"] * 1e-3) / 1e9
-    roof = {"bound": "hbm", "kernel": "gate/up projection + SwiGLU (k_gemm_bf16 EPI_SILU)",
+    step_gbs = sb["total"] / (ms * 1e-3) / 1e9
+    roof = {"bound": "hbm", "kernel": "gate/up projection + SwiGLU (k_gemm_ring, EPI_SILU)",
             "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(wl.name),
             "bytes_per_launch": gu_bytes, "avg_launch_ms": round(gu["isolated_avg_ms"], 5),
             "avg_launch_ms_in_step": round(gu["avg_ms"], 5),
             "timing": ("HIP events around every layer's gate/up launch replayed back to back "
                        "(dsi_profile_kernel, 5 rounds x all layers); in_step: event pair per launch "
-                       "inside the timed steps, which adds the dispatch latency")}
+                       "inside the timed steps, which adds the dispatch latency"),
+            # the whole verification step (every kernel, all algorithmic
+            # bytes) against the same peak; the step is what has to stream at
+            # the roofline, the dominant kernel above is one part of it
+            "step": {"achieved": round(step_gbs, 1), "frac": round(step_gbs / HBM_PEAK_GBS, 4),
+                     "target_frac": 0.70, "ms_at_target": round(sb["total"] / (0.70 * HBM_PEAK_GBS * 1e9) * 1e3, 4),
+                     "bytes": sb["total"]}}
     out = {
         "metric": METRIC,
         "value": round(B * k / (ms * 1e-3), 1),
@@ -603,8 +610,8 @@ def main():
                        "p50": round(float(np.percentile(g["per_step"], 50)), 4),
                        "p90": round(float(np.percentile(g["per_step"], 90)), 4)},
         "step_hbm": {"algorithmic_bytes": sb["total"],
-                     "achieved_GBs": round(sb["total"] / (ms * 1e-3) / 1e9, 1),
-                     "frac_of_peak": round(sb["total"] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
+                     "achieved_GBs": round(step_gbs, 1),
+                     "frac_of_peak": round(step_gbs / HBM_PEAK_GBS, 4)},
         "stream_copy": {"GBs": round(g["copy_GBs"], 1), "bytes": 2 << 30,
                         "step_frac_of_copy": round(sb["total"] / (ms * 1e-3) / 1e9 / g["copy_GBs"], 4)},
         "kernels_ms_per_step": {n: round(v["ms_per_step"], 4) for n, v in g["kernels"].items()},

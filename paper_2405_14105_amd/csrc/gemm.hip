@@ -266,17 +266,16 @@ __device__ __forceinline__ void row_scales(const GemmArgs& a, const SsqIn& pre, 
 // workgroup counts its arrival (a device-scope atomic), and the last arrival
 // reads the partials with device-scope loads, so partials written from
 // another XCD are seen without a write-back or invalidation of any L2.
-// Items are 4 consecutive features of one row, one item per thread (at most
-// MT*16 rows x NBW n-blocks x 4 <= NW*64); the four lanes of one (row,
-// n-block) are adjacent, so the n-block's sum of squares is a two-step
-// butterfly.  The residual and gain values of the thread's item are loaded
-// at the start of the kernel (fold_prefetch), off the critical path.
+// Items are 4 consecutive features of one row (rows x n-blocks x 4 of
+// them), taken by the threads in rounds of the workgroup size; the four
+// lanes of one (row, n-block) are adjacent, so the n-block's sum of squares
+// is a two-step butterfly.  The residual and gain values of each thread's
+// first item are loaded at the start of the kernel (fold_prefetch), off the
+// critical path.
 struct FoldIn {
   float4 x, g;
 };
-template <int MT, int NBW, int NW>
 __device__ __forceinline__ FoldIn fold_prefetch(const GemmArgs& a, int nb0, int nbv) {
-  static_assert(MT * NBW <= NW, "one fold item per thread");
   FoldIn f{};
   const int it = threadIdx.x;
   if (it < a.M * nbv * 4) {
@@ -299,9 +298,10 @@ __device__ __forceinline__ void part_fold(const GemmArgs& a, int nb0, int nbv, c
     s_last = __hip_atomic_fetch_add(e.cnt + g, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == a.S - 1;
   __syncthreads();
   if (!s_last) return;
-  {
-    const int it = threadIdx.x;
-    const bool ok = it < a.M * nbv * 4;
+  const int total = a.M * nbv * 4;
+  for (int base = 0; base < total; base += NW * 64) {   // uniform trip count
+    const int it = base + threadIdx.x;
+    const bool ok = it < total;
     const int q = it & 3, jm = it >> 2;
     const int m = ok ? jm / nbv : 0, nb = nb0 + (ok ? jm % nbv : 0);
     const int n0 = nb * 16 + q * 4;
@@ -317,7 +317,11 @@ __device__ __forceinline__ void part_fold(const GemmArgs& a, int nb0, int nbv, c
 #pragma unroll
         for (int c = 0; c < 4; ++c) pv[sp][c] = __hip_atomic_load(pp + c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
-      float4 xv = pre.x;
+      float4 xv = pre.x, gv = pre.g;
+      if (base > 0) {
+        xv = *(const float4*)(e.x + (size_t)m * e.ld + n0);
+        gv = *(const float4*)(e.gain + n0);
+      }
 #pragma unroll
       for (int sp = 0; sp < kMaxSplits; ++sp) {
         if (sp < a.S) {
@@ -329,7 +333,6 @@ __device__ __forceinline__ void part_fold(const GemmArgs& a, int nb0, int nbv, c
       }
       *(float4*)(e.x + (size_t)m * e.ld + n0) = xv;
       if (e.copy) *(float4*)(e.copy + (size_t)m * e.ld + n0) = xv;
-      const float4 gv = pre.g;
       const float y[4] = {xv.x * gv.x, xv.y * gv.y, xv.z * gv.z, xv.w * gv.w};
       pack_store4(e.pack, WT, m, n0, y);
       sq = xv.x * xv.x + xv.y * xv.y + xv.z * xv.z + xv.w * xv.w;
@@ -492,7 +495,7 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_bf16(GemmArgs a) {
   const SsqIn spre = ssq_prefetch<EPI>(a);
   const EpiIn pre = epi_prefetch<MT, NBW, NW, EPI>(a, nb0);
   FoldIn fpre{};
-  if constexpr (EPI == EPI_PARTRES) fpre = fold_prefetch<MT, NBW, NW>(a, nb0, nbv);
+  if constexpr (EPI == EPI_PARTRES) fpre = fold_prefetch(a, nb0, nbv);
   if constexpr (kPipelined<MT, EPI>) {
     if (nk > 0) {
       // two weight register sets used in turn (a copy from one to the other
@@ -608,7 +611,7 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_f32(GemmArgs a) {
   const float4* __restrict__ X = (const float4*)a.Xhi;
   const EpiIn pre = epi_prefetch<MT, NBW, NW, EPI>(a, nb0);
   FoldIn fpre{};
-  if constexpr (EPI == EPI_PARTRES) fpre = fold_prefetch<MT, NBW, NW>(a, nb0, nbv);
+  if constexpr (EPI == EPI_PARTRES) fpre = fold_prefetch(a, nb0, nbv);
   if (a.ssq) row_scales<NW>(a, ssq_prefetch<EPI>(a), rs);
 
   f32x4 acc[NBW][MT];
@@ -668,8 +671,19 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_f32(GemmArgs a) {
 // epilogues as the packed kernel.
 constexpr int kRingDepth = 8;
 
-// RMSNorm sums of rows w and w + kRingWaves (every row of a 16-row tile),
-// requested before the weights and reduced after the main loop
+// Weight tiles in flight per wave for MT row tiles: 8, or 4 where the
+// registers would not hold 8 -- the narrow roles (one or two n-blocks per
+// workgroup) with several row tiles, whose activation slots (hi and lo of MT
+// tiles per k-block in flight) grow with MT, and gate/up's 7 x 4 accumulator
+// tiles at four row tiles.  The depth does not change any sum.
+constexpr int ring_depth(int nbw, int mt) { return ((mt > 1 && nbw <= 2) || (mt >= 4 && nbw >= 7)) ? 4 : kRingDepth; }
+// n-blocks per LDS reduction round: kRingWaves x NBR x MT tiles of 1 KB
+// within 128 KB
+constexpr int ring_red_nb(int nbw, int mt) { return 16 / mt < nbw ? 16 / mt : nbw; }
+
+// RMSNorm sums of rows w and w + kRingWaves (the first 16 rows), requested
+// before the weights and reduced after the main loop; rows beyond 16 (wave
+// w: rows w + 8h) are loaded after it
 struct RingSsq {
   float v[2][kSsqPer];
 };
@@ -698,29 +712,49 @@ __device__ __forceinline__ RingSsq ring_ssq_prefetch(const GemmArgs& a) {
   return r;
 }
 
+// rs[m] = 1/sqrt(sum / d + eps) for the MT*16 rows; row m is reduced by wave
+// m % 8 in the same order for every MT (lane entries, then a butterfly)
+template <int MT>
 __device__ __forceinline__ void ring_row_scales(const GemmArgs& a, const RingSsq& pre, float* rs) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
+  for (int h = 0; h < 2 * MT; ++h) {
     const int m = w + h * kRingWaves;
+    float v[kSsqPer];
+#pragma unroll
+    for (int c = 0; c < kSsqPer; ++c) {
+      if (h < 2) {
+        v[c] = pre.v[h < 2 ? h : 0][c];
+      } else {
+        v[c] = 0.f;
+        if (m < a.M && lane + 64 * c < a.ssq_n) v[c] = a.ssq[(size_t)m * a.ssq_n + lane + 64 * c];
+      }
+    }
     float sum = 0.f;
 #pragma unroll
-    for (int c = 0; c < kSsqPer; ++c) sum += pre.v[h][c];
+    for (int c = 0; c < kSsqPer; ++c) sum += v[c];
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) sum += __shfl_xor(sum, off);
     if (lane == 0 && m < a.M) rs[m] = 1.0f / sqrtf(sum / (float)a.norm_d + a.eps);
   }
 }
 
-template <int NK, int NBW, int EPI>
+// MT row tiles (1..4) of the activation pack; every row's sums are formed
+// in the same order for every MT -- each wave's k-blocks in order, hi then
+// lo, the waves reduced in order -- so a row's results do not depend on
+// how many rows share the launch.
+template <int NK, int NBW, int EPI, int MT>
 __global__ __launch_bounds__(kRingWaves * 64) void k_gemm_ring(GemmArgs a) {
-  constexpr int NW = kRingWaves, D = kRingDepth, N = NK * NBW;
+  constexpr int NW = kRingWaves, D = ring_depth(NBW, MT), N = NK * NBW;
   // activation slots: k-block i's fragments are requested together with its
-  // first weight tile (D tiles ahead of use) and live until its last tile
-  constexpr int A = (D + NBW - 1) / NBW + 1;
+  // first weight tile (D tiles ahead of use) and live until its last tile;
+  // when one is requested, tile u has just been consumed and tiles
+  // u+1 .. u+D-1 still need ceil((D-1)/NBW) k-blocks
+  constexpr int A = (D - 1 + NBW - 1) / NBW + 1;
+  constexpr int NBR = ring_red_nb(NBW, MT);
   static_assert(N >= D, "a wave's run must fill the ring");
-  __shared__ f32x4 red[NW * NBW * 64];
-  __shared__ float rs[16];
+  __shared__ f32x4 red[NW * NBR * MT * 64];
+  __shared__ float rs[MT * 16];
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int g = blockIdx.x / a.S, split = blockIdx.x - g * a.S;
@@ -731,28 +765,30 @@ __global__ __launch_bounds__(kRingWaves * 64) void k_gemm_ring(GemmArgs a) {
   // activation packs as buffers: a lane whose token row is padding (>= M)
   // or whose k-block lies past the matrix reads out of range, which returns
   // zeros without a memory access
-  const int nrec = a.Kb * 1024;
+  const int nrec = MT * a.Kb * 1024;
   const __amdgpu_buffer_rsrc_t Rh = __builtin_amdgcn_make_buffer_rsrc((void*)a.Xhi, (short)0, nrec, 0x00020000);
   const __amdgpu_buffer_rsrc_t Rl = __builtin_amdgcn_make_buffer_rsrc((void*)a.Xlo, (short)0, nrec, 0x00020000);
-  const bool row_ok = (lane & 15) < a.M;
-  auto xoff = [&](int i) -> int {
-    return (row_ok && kb0 + i < a.Kb) ? ((kb0 + i) * 64 + lane) * 16 : 0x7ffffff0;
+  auto xoff = [&](int i, int t) -> int {
+    return ((lane & 15) + 16 * t < a.M && kb0 + i < a.Kb) ? ((t * a.Kb + kb0 + i) * 64 + lane) * 16 : 0x7ffffff0;
   };
 
-  const EpiIn pre = epi_prefetch<1, NBW, NW, EPI>(a, nb0);
+  const EpiIn pre = epi_prefetch<MT, NBW, NW, EPI>(a, nb0);
   FoldIn fpre{};
-  if constexpr (EPI == EPI_PARTRES) fpre = fold_prefetch<1, NBW, NW>(a, nb0, nbv);
+  if constexpr (EPI == EPI_PARTRES) fpre = fold_prefetch(a, nb0, nbv);
   const RingSsq spre = ring_ssq_prefetch<EPI>(a);
   __builtin_amdgcn_sched_barrier(0);
   u32x4 ring[D];
-  u32x4 xh[A], xl[A];
+  u32x4 xh[A][MT], xl[A][MT];
   // issue position u: the fragments of k-block u / NBW when u starts one,
   // then weight tile u
   auto issue = [&](int u) {
     if (u % NBW == 0) {
       const int i = u / NBW;
-      xh[i % A] = __builtin_amdgcn_raw_buffer_load_b128(Rh, xoff(i), 0, 0);
-      xl[i % A] = __builtin_amdgcn_raw_buffer_load_b128(Rl, xoff(i), 0, 0);
+#pragma unroll
+      for (int t = 0; t < MT; ++t) {
+        xh[i % A][t] = __builtin_amdgcn_raw_buffer_load_b128(Rh, xoff(i, t), 0, 0);
+        xl[i % A][t] = __builtin_amdgcn_raw_buffer_load_b128(Rl, xoff(i, t), 0, 0);
+      }
     }
     ring[u % D] = __builtin_nontemporal_load(Ws + (size_t)u * 64);
   };
@@ -761,23 +797,35 @@ __global__ __launch_bounds__(kRingWaves * 64) void k_gemm_ring(GemmArgs a) {
     issue(r);
     __builtin_amdgcn_sched_barrier(0);   // issue order = ring order
   }
-  f32x4 acc[NBW];
+  f32x4 acc[NBW][MT];
 #pragma unroll
-  for (int j = 0; j < NBW; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int j = 0; j < NBW; ++j)
+#pragma unroll
+    for (int t = 0; t < MT; ++t) acc[j][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int u = 0; u < N; ++u) {
     const bf16x8 wv = as_bf16x8(ring[u % D]);
     const int i = u / NBW;
-    acc[u % NBW] = mfma_bf16(wv, as_bf16x8(xh[i % A]), acc[u % NBW]);
-    acc[u % NBW] = mfma_bf16(wv, as_bf16x8(xl[i % A]), acc[u % NBW]);
+#pragma unroll
+    for (int t = 0; t < MT; ++t) {
+      acc[u % NBW][t] = mfma_bf16(wv, as_bf16x8(xh[i % A][t]), acc[u % NBW][t]);
+      acc[u % NBW][t] = mfma_bf16(wv, as_bf16x8(xl[i % A][t]), acc[u % NBW][t]);
+    }
     if (u + D < N) issue(u + D);
     __builtin_amdgcn_sched_barrier(0);   // consume tile u, then refill its slot
   }
-  if (a.ssq) ring_row_scales(a, spre, rs);
+  if (a.ssq) ring_row_scales<MT>(a, spre, rs);
 #pragma unroll
-  for (int j = 0; j < NBW; ++j) red[(w * NBW + j) * 64 + lane] = acc[j];
-  __syncthreads();
-  finish<W_BF16, EPI, 1, NBW, NW>(a, red, a.ssq ? rs : nullptr, nb0, NBW, split, pre);
+  for (int j0 = 0; j0 < NBW; j0 += NBR) {
+    if (j0 > 0) __syncthreads();   // the previous round's tiles have been read
+#pragma unroll
+    for (int jj = 0; jj < NBR; ++jj)
+#pragma unroll
+      for (int t = 0; t < MT; ++t)
+        if (j0 + jj < NBW) red[((w * NBR + jj) * MT + t) * 64 + lane] = acc[j0 + jj][t];
+    __syncthreads();
+    finish<W_BF16, EPI, MT, NBR, NW>(a, red, a.ssq ? rs : nullptr, nb0 + j0, min(NBR, NBW - j0), split, pre);
+  }
   if constexpr (EPI == EPI_PARTRES) part_fold<W_BF16, NW>(a, nb0, nbv, fpre);
 }
 
@@ -810,27 +858,38 @@ struct RingRole<EPI_PARTRES> : RingRole<EPI_PART> {};
 // is rounded up to one of them; the extra tiles are zero)
 constexpr int kRingNk[] = {1, 2, 4, 8, 14, 16};
 
-template <int EPI, int NK>
+template <int EPI, int NK, int MT>
 hipError_t launch_ring_nk(const GemmArgs& a, hipStream_t s) {
   constexpr int NBW = RingRole<EPI>::NBW;
   if constexpr (NK * NBW < kRingDepth) {
     return hipErrorInvalidValue;
   } else {
     const int grid = ((a.Nb + NBW - 1) / NBW) * a.S;
-    hipLaunchKernelGGL((k_gemm_ring<NK, NBW, EPI>), dim3(grid), dim3(kRingWaves * 64), 0, s, a);
+    hipLaunchKernelGGL((k_gemm_ring<NK, NBW, EPI, MT>), dim3(grid), dim3(kRingWaves * 64), 0, s, a);
     return hipGetLastError();
   }
 }
 
-template <int EPI>
-hipError_t launch_ring(const GemmArgs& a, hipStream_t s) {
+template <int EPI, int MT>
+hipError_t launch_ring_mt(const GemmArgs& a, hipStream_t s) {
   switch (a.ring_nk) {
-    case 1: return launch_ring_nk<EPI, 1>(a, s);
-    case 2: return launch_ring_nk<EPI, 2>(a, s);
-    case 4: return launch_ring_nk<EPI, 4>(a, s);
-    case 8: return launch_ring_nk<EPI, 8>(a, s);
-    case 14: return launch_ring_nk<EPI, 14>(a, s);
-    case 16: return launch_ring_nk<EPI, 16>(a, s);
+    case 1: return launch_ring_nk<EPI, 1, MT>(a, s);
+    case 2: return launch_ring_nk<EPI, 2, MT>(a, s);
+    case 4: return launch_ring_nk<EPI, 4, MT>(a, s);
+    case 8: return launch_ring_nk<EPI, 8, MT>(a, s);
+    case 14: return launch_ring_nk<EPI, 14, MT>(a, s);
+    case 16: return launch_ring_nk<EPI, 16, MT>(a, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+template <int EPI>
+hipError_t launch_ring(const GemmArgs& a, int mt, hipStream_t s) {
+  switch (mt) {
+    case 1: return launch_ring_mt<EPI, 1>(a, s);
+    case 2: return launch_ring_mt<EPI, 2>(a, s);
+    case 3: return launch_ring_mt<EPI, 3>(a, s);
+    case 4: return launch_ring_mt<EPI, 4>(a, s);
   }
   return hipErrorInvalidValue;
 }
@@ -1021,13 +1080,13 @@ hipError_t launch_restream(const void* src, int Nb, int Kb, int G, const RingCfg
 
 hipError_t launch_gemm(int wtype, int mt, const GemmArgs& a, hipStream_t s) {
   if (a.Nb <= 0 || a.M <= 0) return hipSuccess;
-  if (a.Ws && mt == 1 && wtype == W_BF16 && a.M <= 16) {
+  if (a.Ws && wtype == W_BF16 && mt >= 1 && mt <= kMaxMt && a.M <= 16 * mt) {
     switch (a.epi.kind) {
-      case EPI_QKV: return launch_ring<EPI_QKV>(a, s);
-      case EPI_RESID: return launch_ring<EPI_RESID>(a, s);
-      case EPI_SILU: return launch_ring<EPI_SILU>(a, s);
-      case EPI_PART: return launch_ring<EPI_PART>(a, s);
-      case EPI_PARTRES: return launch_ring<EPI_PARTRES>(a, s);
+      case EPI_QKV: return launch_ring<EPI_QKV>(a, mt, s);
+      case EPI_RESID: return launch_ring<EPI_RESID>(a, mt, s);
+      case EPI_SILU: return launch_ring<EPI_SILU>(a, mt, s);
+      case EPI_PART: return launch_ring<EPI_PART>(a, mt, s);
+      case EPI_PARTRES: return launch_ring<EPI_PARTRES>(a, mt, s);
     }
     return hipErrorInvalidValue;
   }

@@ -408,12 +408,14 @@ dsi_status plan_attention(dsi_model* m, dsi_kv* kv, int window0, int B, int R, A
   return DSI_OK;
 }
 
-// Whether a forward runs its layer GEMMs on the ring layouts: one row tile
-// (at most 16 rows) on a cache of one window.  A cache of several windows
-// (verification tasks batched together) always takes the packed kernels, so
-// a window gives bit-identical results alone or inside a batch of its cache.
+// Whether a forward runs its layer GEMMs on the ring layouts: every bf16
+// forward of a model built with them (one to four row tiles, any number of
+// windows).  The ring kernels form each row's sums in the same order for
+// every row count, so a window's results are the same alone or inside a
+// batch.
 bool ring_forward(const dsi_model* m, const dsi_kv* kv, int mt) {
-  return m->use_ring && m->wtype == W_BF16 && mt == 1 && kv->n_windows == 1;
+  (void)kv;
+  return m->use_ring && m->wtype == W_BF16 && mt >= 1 && mt <= kMaxMt;
 }
 
 // Stream-ordered launches only (capturable into a graph).  depth / anc

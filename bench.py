@@ -32,8 +32,8 @@ METRIC = "verify-step latency (ms) + verified draft tokens/s, 8B-shape k=10; % H
 # profiles/verify_8b_k10_hbm_traffic.md (FETCH_SIZE x 2.0 + WRITE_SIZE x 1.0,
 # scales from a 512 MiB copy).  Reported only while the GEMM sources are the
 # ones the counters were taken with.
-TRAFFIC_MEASURED = {"workload": "llama8b_L2048_k10", "bytes": 237.89e6,
-                    "sources_sha256": "2cd6fb2ccddb64c6dcc5b5dae25a34a2a970a695ba7cf43c05dece7900ff6325"}
+TRAFFIC_MEASURED = {"workload": "llama8b_L2048_k10", "bytes": 237.88e6,
+                    "sources_sha256": "680c0a30a03ff4432fd278d53aade1ec24944bdee1e02fa0af9e057d33736b14"}
 GEMM_SOURCES = ("paper_2405_14105_amd/csrc/gemm.hip", "paper_2405_14105_amd/csrc/device_util.h",
                 "paper_2405_14105_amd/csrc/internal.h")
 HBM_PEAK_GBS = 8000.0

@@ -832,7 +832,7 @@ __global__ __launch_bounds__(kRingWaves * 64) void k_gemm_ring(GemmArgs a) {
 // n-blocks per workgroup of each role's ring layout: the O projection one
 // (256 workgroups at d = 4096), QKV two (192 at the 8B shape), gate/up
 // seven (one workgroup per CU for 1792 n-blocks), the down projection four
-// with its K split (as the packed launch)
+// with its K split (as the packed launch), the LM head eight
 template <int EPI>
 struct RingRole;
 template <>
@@ -853,6 +853,10 @@ struct RingRole<EPI_PART> {
 };
 template <>
 struct RingRole<EPI_PARTRES> : RingRole<EPI_PART> {};
+template <>
+struct RingRole<EPI_STORE> {   // the LM head: many rounds of workgroups
+  static constexpr int NBW = 8;
+};
 
 // k-blocks per wave the ring kernel is built for (a shape's k-range per wave
 // is rounded up to one of them; the extra tiles are zero)
@@ -1051,6 +1055,7 @@ bool ring_config(int wtype, int epi_kind, int Nb, int Kb, int S, RingCfg* out) {
     case EPI_SILU: nbw = RingRole<EPI_SILU>::NBW; break;
     case EPI_PART:
     case EPI_PARTRES: nbw = RingRole<EPI_PART>::NBW; break;
+    case EPI_STORE: nbw = RingRole<EPI_STORE>::NBW; break;
     default: return false;
   }
   if (S > 1 && epi_kind != EPI_PART && epi_kind != EPI_PARTRES) return false;
@@ -1087,6 +1092,7 @@ hipError_t launch_gemm(int wtype, int mt, const GemmArgs& a, hipStream_t s) {
       case EPI_SILU: return launch_ring<EPI_SILU>(a, mt, s);
       case EPI_PART: return launch_ring<EPI_PART>(a, mt, s);
       case EPI_PARTRES: return launch_ring<EPI_PARTRES>(a, mt, s);
+      case EPI_STORE: return launch_ring<EPI_STORE>(a, mt, s);
     }
     return hipErrorInvalidValue;
   }

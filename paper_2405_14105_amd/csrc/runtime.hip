@@ -99,11 +99,12 @@ struct dsi_model {
   int G_gu = 1, G_head = 1;   // n-block groups of the packed gate/up and LM head
   // ring layouts of the four layer GEMMs (nbw == 0: the role has none) and
   // whether one-row-tile forwards on single-window caches use them
-  RingCfg rc_qkv, rc_o, rc_gu, rc_down;
+  RingCfg rc_qkv, rc_o, rc_gu, rc_down, rc_head;
   bool use_ring = true;
   void* embed = nullptr;
   float* final_norm = nullptr;
   void* lm_head = nullptr;
+  void* lm_head_s = nullptr;   // the LM head in the ring layout (nullable)
   std::vector<LayerW> layers;
   std::vector<unsigned> set_mask;   // [L+1]: bit per tensor id (index 0: globals)
   std::vector<void*> allocs;
@@ -344,11 +345,12 @@ GemmArgs down_args(dsi_model* m, int l, int M, int mt, float* hidden_next = null
   return g;
 }
 
-GemmArgs head_args(dsi_model* m, float* logits, int M) {
+GemmArgs head_args(dsi_model* m, float* logits, int M, bool ring = false) {
   GemmArgs g{};
   g.M = M;
   g.S = 1;
   g.W = m->lm_head;
+  set_ring(g, m->rc_head, m->lm_head_s, ring);
   g.Xhi = m->pk_d.hi;
   g.Xlo = m->pk_d.lo;
   g.Nb = m->Nb_head;
@@ -510,7 +512,7 @@ dsi_status run_forward(dsi_model* m, dsi_kv* kv, const AttnPlan& ap, int window0
     return DSI_OK;
   }
 
-  GemmArgs gh = head_args(m, logits, M);
+  GemmArgs gh = head_args(m, logits, M, ring);
   Prof ph(m, DSI_K_HEAD);
   if (head_last_only) {
     const size_t off = (size_t)(M - 1) * m->d;
@@ -693,6 +695,7 @@ dsi_status dsi_model_create(const dsi_config* cfg, void* stream, dsi_model** out
   ring_config(m->wtype, EPI_QKV, m->Nb_qkv, m->Kb_d, 1, &m->rc_qkv);
   ring_config(m->wtype, EPI_RESID, m->Nb_o, m->Kb_q, 1, &m->rc_o);
   ring_config(m->wtype, EPI_SILU, m->Nb_gu, m->Kb_d, 1, &m->rc_gu);
+  ring_config(m->wtype, EPI_STORE, m->Nb_head, m->Kb_d, 1, &m->rc_head);
   ring_config(m->wtype, EPI_PARTRES, m->Nb_down, m->Kb_ff,
               gemm_part_splits(m->wtype, m->Nb_down, m->Kb_ff, 1), &m->rc_down);
   m->layers.resize(m->L);
@@ -706,6 +709,7 @@ dsi_status dsi_model_create(const dsi_config* cfg, void* stream, dsi_model** out
   A(&m->embed, (size_t)m->V * m->d * m->esz);
   A((void**)&m->final_norm, (size_t)m->d * 4);
   A(&m->lm_head, (size_t)m->Nb_head * m->Kb_d * tile * m->esz);
+  if (m->use_ring && m->rc_head.nbw) A(&m->lm_head_s, m->rc_head.tiles() * tile * m->esz);
   for (int l = 0; l < m->L && st == DSI_OK; ++l) {
     LayerW& w = m->layers[l];
     A((void**)&w.attn_norm, (size_t)m->d * 4);
@@ -855,6 +859,11 @@ dsi_status dsi_model_set_tensor(dsi_model* m, int32_t layer, int32_t id, const v
     if (e != hipSuccess) return fail(DSI_EHIP, "prepack: %s", hipGetErrorString(e));
   }
   m->set_mask[global ? 0 : layer + 1] |= 1u << id;
+  if (id == DSI_T_LM_HEAD && m->lm_head_s) {
+    hipError_t e = launch_restream(m->lm_head, m->Nb_head, m->Kb_d, m->G_head, m->rc_head, m->lm_head_s, nullptr);
+    if (e == hipSuccess) e = hipDeviceSynchronize();
+    if (e != hipSuccess) return fail(DSI_EHIP, "ring layout: %s", hipGetErrorString(e));
+  }
   if (!global) {
     // once every part of a role's matrix is packed, lay it out for the ring
     // kernel as well
@@ -1282,7 +1291,7 @@ dsi_status dsi_profile_kernel(dsi_model* m, dsi_kv* kv, int32_t cls, int32_t rou
       case DSI_K_OPROJ: g = oproj_args(m, l, M, ring); break;
       case DSI_K_GATEUP: g = gateup_args(m, l, M, ring); break;
       case DSI_K_DOWN: g = down_args(m, l, M, mt, nullptr, ring); break;
-      default: g = head_args(m, m->logits, M); break;
+      default: g = head_args(m, m->logits, M, ring); break;
     }
     HIP_TRY(launch_gemm(m->wtype, mt, g, s));
     return DSI_OK;

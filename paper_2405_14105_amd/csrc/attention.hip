@@ -9,8 +9,10 @@
 // n_kv query heads times R window rows form the query side; they are cut
 // into tiles of 16 queries.  Per 32-key step a wavefront computes
 //   S^T[key][query] = K . Q^T     (A = 16 K rows, B = Q^T hi/lo)
-//   O^T[d][query]  += V^T . P^T   (A = V^T rows of the blocked, transposed
-//                                  value cache: 8 contiguous KB per step)
+//   O^T[d][query]  += V^T . P^T   (A = V^T rows)
+// on the cache's 32-position blocks (kc_off / vc_off): the keys and the
+// values of one step are each one contiguous block (8 KB at hd = 128) and
+// every fragment load reads whole 128-byte lines
 // with 16x16x32 bf16 MFMAs (two per product for the hi/lo query or
 // probability split), so every operand is a 16-byte lane load and the
 // query owned by a lane (l % 16) is the same in S^T, P^T and O^T: the
@@ -28,15 +30,16 @@ namespace {
 
 // PIPE: each wave handles several 32-key steps (long prefixes); the loads
 // of its next step are issued as soon as the current step's K (after S) and
-// V (after O) fragments have been consumed, so they overlap the math.  With
-// PIPE == 2 two register sets alternate and each is refilled with the step
-// two ahead, doubling the bytes in flight per wave.
+// V (after O) fragments have been consumed, so they overlap the math.
+// NTL: keys and values read by this workgroup only (one query tile) are
+// loaded nontemporally, streaming them past the caches: a long prefix then
+// reads at ~6.7-7.0 instead of ~5.6-5.9 TB/s.
 // TREE: token-tree rows -- a window key L + j is visible to query row i only
 // if node j is an ancestor of node i (or i itself), per AttnArgs::anc.
 // NWV: waves per workgroup, 8, or 4 (many windows in flight: more, smaller
 // workgroups), for bf16 caches with registers capped so that three
 // workgroups share a CU.
-template <int KVB, int HD, int PIPE, int TREE, int NWV>
+template <int KVB, int HD, int PIPE, int TREE, int NWV, int NTL>
 __global__ __launch_bounds__(NWV * 64, (NWV == 4 && KVB) ? 3 : 1) void k_attn(AttnArgs a) {
   constexpr int DS = HD / 32;
   constexpr int DT = HD / 16;
@@ -79,15 +82,14 @@ __global__ __launch_bounds__(NWV * 64, (NWV == 4 && KVB) ? 3 : 1) void k_attn(At
   const int r16 = lane & 15;
   const int kgrp = (lane >> 4) * 8;
 
-  // K and V of one 32-key step; PIPE == 2 keeps a second set for the step
-  // after the next (bf16 caches only)
+  // K and V of one 32-key step
   struct KV16 {
     u32x4 k[2][DS], v[DT];
   };
   struct KV32 {
     F8 k[2][DS], v[DT];
   };
-  KV16 b16, b16n;
+  KV16 b16;
   KV32 b32;
   auto load_k_into = [&](KV16& d16, KV32& d32, int p0) {
 #pragma unroll
@@ -95,9 +97,10 @@ __global__ __launch_bounds__(NWV * 64, (NWV == 4 && KVB) ? 3 : 1) void k_attn(At
       const int key = p0 + (r16 >> 2) * 8 + t * 4 + (r16 & 3);
 #pragma unroll
       for (int ds = 0; ds < DS; ++ds) {
-        const size_t kidx = kbase + (size_t)key * HD + ds * 32 + kgrp;
+        const size_t kidx = kbase + kc_off(key, ds * 32 + kgrp, HD);
         if (KVB) {
-          d16.k[t][ds] = *(const u32x4*)((const uint16_t*)a.kc + kidx);
+          const u32x4* src = (const u32x4*)((const uint16_t*)a.kc + kidx);
+          d16.k[t][ds] = NTL ? __builtin_nontemporal_load(src) : *src;
         } else {
           d32.k[t][ds].a = *(const float4*)((const float*)a.kc + kidx);
           d32.k[t][ds].b = *(const float4*)((const float*)a.kc + kidx + 4);
@@ -108,10 +111,11 @@ __global__ __launch_bounds__(NWV * 64, (NWV == 4 && KVB) ? 3 : 1) void k_attn(At
   auto load_v_into = [&](KV16& d16, KV32& d32, int p0) {
 #pragma unroll
     for (int t = 0; t < DT; ++t) {
-      // 32-key block p0/32 of the blocked V^T cache: dims x 32 keys, contiguous
-      const size_t vidx = vbase + ((size_t)(p0 >> 5) * HD + t * 16 + r16) * 32 + kgrp;
+      // dims t*16 + r16 of the step's block, keys kgrp .. kgrp + 7
+      const size_t vidx = vbase + vc_off(p0 + kgrp, t * 16 + r16, HD);
       if (KVB) {
-        d16.v[t] = *(const u32x4*)((const uint16_t*)a.vc + vidx);
+        const u32x4* src = (const u32x4*)((const uint16_t*)a.vc + vidx);
+        d16.v[t] = NTL ? __builtin_nontemporal_load(src) : *src;
       } else {
         d32.v[t].a = *(const float4*)((const float*)a.vc + vidx);
         d32.v[t].b = *(const float4*)((const float*)a.vc + vidx + 4);
@@ -147,10 +151,6 @@ __global__ __launch_bounds__(NWV * 64, (NWV == 4 && KVB) ? 3 : 1) void k_attn(At
   const int plim = min(c0 + a.chunk, a.maxlen);
   load_k_into(b16, b32, max(0, min(pfirst, plim - 32)));
   load_v_into(b16, b32, max(0, min(pfirst, plim - 32)));
-  if constexpr (PIPE == 2) {
-    load_k_into(b16n, b32, max(0, min(pfirst + stride, plim - 32)));
-    load_v_into(b16n, b32, max(0, min(pfirst + stride, plim - 32)));
-  }
   __builtin_amdgcn_sched_barrier(0);   // issue them here, not next to their use
   bf16x8 qh[DS], ql[DS];
   if (KVB) {
@@ -274,16 +274,7 @@ __global__ __launch_bounds__(NWV * 64, (NWV == 4 && KVB) ? 3 : 1) void k_attn(At
     if (pnext >= 0 && pnext < c1) load_v_into(d16, d32, pnext);
   };
 
-  if constexpr (PIPE == 2) {
-    // two register sets, each refilled two steps ahead
-    static_assert(KVB, "two-deep pipelining is built for bf16 caches");
-    for (int p0 = pfirst; p0 < c1; p0 += 2 * stride) {
-      step(p0, b16, b32, p0 + 2 * stride);
-      const int p1 = p0 + stride;
-      if (p1 >= c1) break;
-      step(p1, b16n, b32, p1 + 2 * stride);
-    }
-  } else if constexpr (PIPE == 1) {
+  if constexpr (PIPE == 1) {
     for (int p0 = pfirst; p0 < c1; p0 += stride) step(p0, b16, b32, p0 + stride);
   } else if (pfirst < c1) {
     // unpipelined plans have chunk == 32 * NWV (launch_main takes PIPE 0
@@ -420,25 +411,23 @@ void launch_main(const AttnArgs& a, dim3 grid, hipStream_t s) {
   const dim3 blk(NWV * 64);
   const bool pipe = a.chunk > NWV * 32;
   if constexpr (KVB && NWV == kAttnWaves) {
-    // three or more steps per wave: refill two steps ahead
-    if (a.chunk >= 3 * NWV * 32) {
-      if (a.anc)
-        hipLaunchKernelGGL((k_attn<KVB, HD, 2, 1, NWV>), grid, blk, 0, s, a);
-      else
-        hipLaunchKernelGGL((k_attn<KVB, HD, 2, 0, NWV>), grid, blk, 0, s, a);
+    // several steps per wave and one query tile: no other workgroup reads
+    // these keys and values
+    if (pipe && a.n_qtiles == 1 && !a.anc) {
+      hipLaunchKernelGGL((k_attn<KVB, HD, 1, 0, NWV, 1>), grid, blk, 0, s, a);
       return;
     }
   }
   if (a.anc) {
     if (pipe)
-      hipLaunchKernelGGL((k_attn<KVB, HD, 1, 1, NWV>), grid, blk, 0, s, a);
+      hipLaunchKernelGGL((k_attn<KVB, HD, 1, 1, NWV, 0>), grid, blk, 0, s, a);
     else
-      hipLaunchKernelGGL((k_attn<KVB, HD, 0, 1, NWV>), grid, blk, 0, s, a);
+      hipLaunchKernelGGL((k_attn<KVB, HD, 0, 1, NWV, 0>), grid, blk, 0, s, a);
   } else {
     if (pipe)
-      hipLaunchKernelGGL((k_attn<KVB, HD, 1, 0, NWV>), grid, blk, 0, s, a);
+      hipLaunchKernelGGL((k_attn<KVB, HD, 1, 0, NWV, 0>), grid, blk, 0, s, a);
     else
-      hipLaunchKernelGGL((k_attn<KVB, HD, 0, 0, NWV>), grid, blk, 0, s, a);
+      hipLaunchKernelGGL((k_attn<KVB, HD, 0, 0, NWV, 0>), grid, blk, 0, s, a);
   }
 }
 

@@ -202,8 +202,7 @@ __global__ void k_kv_add_checked(int* lens, int window, const int* tokens, int n
   }
 }
 
-// copy [n_kv][len][hd] <-> cache (K [n_kv][maxlen][hd], blocked V^T
-// [n_kv][maxlen/32][hd][32])
+// copy [n_kv][len][hd] <-> cache (n_kv regions of maxlen * hd, kc_off / vc_off)
 template <typename T>
 __global__ void k_kv_copy(int to_cache, T* kc, T* vc, int n_kv, int hd, int maxlen, int len,
                           T* dk, T* dv) {
@@ -213,8 +212,8 @@ __global__ void k_kv_copy(int to_cache, T* kc, T* vc, int n_kv, int hd, int maxl
     const int dd = (int)(i % hd);
     const int p = (int)((i / hd) % len);
     const int h = (int)(i / ((size_t)hd * len));
-    const size_t ki = ((size_t)h * maxlen + p) * hd + dd;
-    const size_t vi = (((size_t)h * (maxlen >> 5) + (p >> 5)) * hd + dd) * 32 + (p & 31);
+    const size_t ki = (size_t)h * maxlen * hd + kc_off(p, dd, hd);
+    const size_t vi = (size_t)h * maxlen * hd + vc_off(p, dd, hd);
     if (to_cache) {
       kc[ki] = dk[i];
       vc[vi] = dv[i];
@@ -227,7 +226,7 @@ __global__ void k_kv_copy(int to_cache, T* kc, T* vc, int n_kv, int hd, int maxl
 
 // NaN into the dead rows [lens[window], maxlen) of one window: one block per
 // (layer, KV head); kc / vc: the window's layer-0 K and V, layer_stride
-// elements apart; V in the blocked layout [head][maxlen/32][hd][32]
+// elements apart (kc_off / vc_off inside a head's region)
 template <typename T>
 __global__ void k_kv_poison(T* kc, T* vc, size_t layer_stride, int n_kv, int hd, int maxlen, const int* lens,
                             int window, T nan) {
@@ -238,8 +237,8 @@ __global__ void k_kv_poison(T* kc, T* vc, size_t layer_stride, int n_kv, int hd,
   const size_t n = (size_t)(maxlen - len) * hd;
   for (size_t i = threadIdx.x; i < n; i += blockDim.x) {
     const int p = len + (int)(i / hd), dd = (int)(i % hd);
-    k[(size_t)p * hd + dd] = nan;
-    v[((size_t)(p >> 5) * hd + dd) * 32 + (p & 31)] = nan;
+    k[kc_off(p, dd, hd)] = nan;
+    v[vc_off(p, dd, hd)] = nan;
   }
 }
 

@@ -167,19 +167,21 @@ __device__ __forceinline__ float epilogue(const EpiArgs& e, int nb, int r0, int 
           qr[ja + 1] = b1;
           qr[ja + 1 + half] = b2;
         } else {
-          const size_t base = (((size_t)win * e.n_kv + h) * e.maxlen + pos) * hd;
+          const size_t base = ((size_t)win * e.n_kv + h) * e.maxlen * hd;
+          const size_t i0 = base + kc_off(pos, ja, hd), i1 = base + kc_off(pos, ja + half, hd);
+          const size_t i2 = base + kc_off(pos, ja + 1, hd), i3 = base + kc_off(pos, ja + 1 + half, hd);
           if (e.kv_bf16) {
-            uint16_t* kc = (uint16_t*)e.kcache + base;
-            kc[ja] = f2bf_bits(a1);
-            kc[ja + half] = f2bf_bits(a2);
-            kc[ja + 1] = f2bf_bits(b1);
-            kc[ja + 1 + half] = f2bf_bits(b2);
+            uint16_t* kc = (uint16_t*)e.kcache;
+            kc[i0] = f2bf_bits(a1);
+            kc[i1] = f2bf_bits(a2);
+            kc[i2] = f2bf_bits(b1);
+            kc[i3] = f2bf_bits(b2);
           } else {
-            float* kc = (float*)e.kcache + base;
-            kc[ja] = a1;
-            kc[ja + half] = a2;
-            kc[ja + 1] = b1;
-            kc[ja + 1 + half] = b2;
+            float* kc = (float*)e.kcache;
+            kc[i0] = a1;
+            kc[i1] = a2;
+            kc[i2] = b1;
+            kc[i3] = b2;
           }
         }
       } else {
@@ -188,8 +190,7 @@ __device__ __forceinline__ float epilogue(const EpiArgs& e, int nb, int r0, int 
         for (int j = 0; j < 4; ++j) {
           const int n = vb * 16 + r0 + j;
           const int h = n / hd, dd = n % hd;
-          const size_t idx = ((((size_t)win * e.n_kv + h) * (e.maxlen >> 5) + (pos >> 5)) * hd + dd) * 32 +
-                             (pos & 31);
+          const size_t idx = ((size_t)win * e.n_kv + h) * e.maxlen * hd + vc_off(pos, dd, hd);
           if (e.kv_bf16) ((uint16_t*)e.vcache)[idx] = f2bf_bits(s[j]);
           else ((float*)e.vcache)[idx] = s[j];
         }

@@ -80,6 +80,18 @@ struct RowMap {         // token row m -> (window, row within window, position)
   const int* depth;
 };
 
+// KV cache of one (layer, window, KV head): a region of maxlen * hd elements
+// in blocks of 32 positions.  K is stored per block as [hd/32][32 positions]
+// [32 dims] and V transposed per block as [hd][32 positions], so the K (and
+// V) fragments of one 32-key attention step are whole 128-byte lines of one
+// contiguous 32 * hd block.  Element offsets of (position p, dim d):
+__host__ __device__ inline size_t kc_off(int p, int d, int hd) {
+  return ((size_t)(p >> 5) * hd + (d & ~31)) * 32 + (size_t)(p & 31) * 32 + (d & 31);
+}
+__host__ __device__ inline size_t vc_off(int p, int d, int hd) {
+  return ((size_t)(p >> 5) * hd + d) * 32 + (p & 31);
+}
+
 struct EpiArgs {
   int kind;
   // EPI_STORE: out [M][ld]; EPI_PART: out [S][part_stride] holding [M][ld]
@@ -89,8 +101,8 @@ struct EpiArgs {
   int n_valid;          // logical N (features) -- outputs beyond are dropped
   // EPI_QKV
   float* q_out;         // [M][n_heads*hd]
-  void* kcache;         // layer base: [windows][n_kv][maxlen][hd]
-  void* vcache;         // layer base: [windows][n_kv][hd][maxlen]
+  void* kcache;         // layer base: [windows][n_kv] regions of maxlen*hd (kc_off)
+  void* vcache;         // layer base: [windows][n_kv] regions of maxlen*hd (vc_off)
   int kv_bf16;
   int n_heads, n_kv, hd, maxlen;
   const float2* rope;   // [M][hd/2] (cos, sin)

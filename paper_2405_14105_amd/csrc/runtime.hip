@@ -385,8 +385,13 @@ dsi_status plan_attention(dsi_model* m, dsi_kv* kv, int window0, int B, int R, A
   const int G = m->hq / m->hkv;
   p->n_qtiles = cdiv(G * R, 16);
   // about two workgroups per CU for one window (a full second round, not a
-  // short tail): at most 512 / (KV heads x query tiles) chunks
-  const int want = std::max(1, 512 / (m->hkv * p->n_qtiles));
+  // short tail): at most 512 / (KV heads x query tiles) chunks, when every
+  // wave takes a single 32-key step (latency-bound); when that still leaves
+  // several steps per wave (long prefixes, bandwidth-bound), at most 256 /
+  // (KV heads x query tiles) chunks: one round of workgroups streams faster
+  // than two
+  const int units = m->hkv * p->n_qtiles;
+  int want = std::max(1, 512 / units);
   auto chunk_of = [&](int w, int q) {
     const int c = (int)round_up((size_t)cdiv(kv->max_len, w), (size_t)q);
     return std::min(std::max(c, q), 16384);
@@ -399,7 +404,11 @@ dsi_status plan_attention(dsi_model* m, dsi_kv* kv, int window0, int B, int R, A
   // The choice depends on the cache's capacity (windows, max_len), never on
   // the call's batch or lengths.
   const int q8 = kAttnWaves * 32;
-  const int chunk8 = chunk_of(want, q8);
+  int chunk8 = chunk_of(want, q8);
+  if (chunk8 > q8) {
+    want = std::max(1, 256 / units);
+    chunk8 = chunk_of(want, q8);
+  }
   const long long full8 = (long long)kv->n_windows * m->hkv * p->n_qtiles * cdiv(kv->max_len, chunk8);
   p->waves = (chunk8 == q8 && full8 > 256) ? 4 : kAttnWaves;
   p->chunk = p->waves == 4 ? chunk_of(2 * want, 4 * 32) : chunk_of(want, q8);

@@ -152,28 +152,24 @@ __global__ __launch_bounds__(256) void k_tcompact(TreeArgs a, T* kc, T* vc, size
   T* K = kc + base + (size_t)h * maxlen * hd;
   T* Vt = vc + base + (size_t)h * hd * maxlen;
   const int cnt = n * hd;
-  // K [maxlen][hd]
   for (int e = threadIdx.x; e < cnt; e += 256) {
     const int i = e / hd + 1, d = e - (i - 1) * hd;
-    st[e] = K[(size_t)(L + path[i]) * hd + d];
+    st[e] = K[kc_off(L + path[i], d, hd)];
   }
   __syncthreads();
   for (int e = threadIdx.x; e < cnt; e += 256) {
     const int i = e / hd + 1, d = e - (i - 1) * hd;
-    K[(size_t)(L + i) * hd + d] = st[e];
-  }
-  __syncthreads();
-  // V^T in 32-position blocks: (p, d) at ((p / 32) * hd + d) * 32 + p % 32
-  for (int e = threadIdx.x; e < cnt; e += 256) {
-    const int i = e / hd + 1, d = e - (i - 1) * hd;
-    const int p = L + path[i];
-    st[e] = Vt[((size_t)(p >> 5) * hd + d) * 32 + (p & 31)];
+    K[kc_off(L + i, d, hd)] = st[e];
   }
   __syncthreads();
   for (int e = threadIdx.x; e < cnt; e += 256) {
     const int i = e / hd + 1, d = e - (i - 1) * hd;
-    const int p = L + i;
-    Vt[((size_t)(p >> 5) * hd + d) * 32 + (p & 31)] = st[e];
+    st[e] = Vt[vc_off(L + path[i], d, hd)];
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < cnt; e += 256) {
+    const int i = e / hd + 1, d = e - (i - 1) * hd;
+    Vt[vc_off(L + i, d, hd)] = st[e];
   }
 }
 

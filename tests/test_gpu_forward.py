@@ -94,27 +94,32 @@ def test_prefill_last_logits(name):
 # Long caches split every (window, KV head) into several key chunks whose
 # partials the combine launch folds; the chunk size follows the cache's
 # capacity and window count (cdiv(max_len, 512 / (KV heads x query tiles))
-# rounded up to whole workgroup steps):
+# rounded up to whole workgroup steps; when that leaves several 32-key steps
+# per wave, cdiv(max_len, 256 / (KV heads x query tiles))):
 #   gqa_hd64, 1 x 1600: 8-wave workgroups, 256-key chunks, 6 chunks, the
 #     last one 26 keys long;
 #   ragged_bf16, 1 x 1600: 5 chunks of 256, 15 query rows in one tile;
 #   gqa_hd64, 8 x 4400: many windows -- 4-wave workgroups with 128-key
 #     chunks (8 chunks), verified on window 5 of the cache;
-#   many_kv, 1 x 6000: 512-key chunks, two 32-key steps per wave;
-#   many_kv, 1 x 9000: 768-key chunks, three steps per wave (two register
-#     sets refilled two steps ahead);
+#   many_kv, 1 x 6000: 768-key chunks, three 32-key steps per wave, two
+#     query tiles;
+#   many_kv, 1 x 9000: 1280-key chunks, five steps per wave;
 #   tiny (fp32 cache), 8 x 2100: the many-window 4-wave plan on an fp32
 #     cache (128-key chunks), window 3;
-#   tiny (fp32 cache), 1 x 33000: 512-key chunks, two steps per wave on
-#     fp32 keys and values.
+#   tiny (fp32 cache), 1 x 33000: 768-key chunks, three steps per wave on
+#     fp32 keys and values;
+#   mha_hd128, 1 x 70000: one query tile with several steps per wave, so the
+#     keys and values are streamed with nontemporal loads (768-key chunks,
+#     three chunks).
 @pytest.mark.parametrize("name,n_windows,max_len,win,L,k", [
     ("gqa_hd64", 1, 1600, 0, 1300, 5),
     ("ragged_bf16", 1, 1600, 0, 1100, 4),
     ("gqa_hd64", 8, 4400, 5, 1000, 5),
     ("many_kv", 1, 6000, 0, 1000, 7),
-    ("many_kv", 1, 9000, 0, 1000, 7),
+    ("many_kv", 1, 9000, 0, 2000, 7),
     ("tiny", 8, 2100, 3, 900, 5),
-    ("tiny", 1, 33000, 0, 700, 5),
+    ("tiny", 1, 33000, 0, 1500, 5),
+    ("mha_hd128", 1, 70000, 0, 2000, 5),
 ])
 def test_multichunk_attention(name, n_windows, max_len, win, L, k):
     shape = S.SHAPES[name]

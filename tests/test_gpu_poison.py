@@ -7,8 +7,8 @@ token tree) run again must give bit-identical, finite logits and the same
 decisions: no kernel reads a row past the window's rows into a result, and
 the masked keys of a partial 32-key step (probability 0) cannot turn a NaN
 value row into a NaN output.  Covers bf16 and fp32 caches, one and several
-key chunks, 4-wave and pipelined attention plans, and the ring O
-projection.
+key chunks, 4-wave and pipelined attention plans (with nontemporal key and
+value loads), and the ring O projection.
 """
 import numpy as np
 import pytest
@@ -25,10 +25,14 @@ SEED = 0
 
 # cap: cache capacity (None: the window plus slack).  gqa_hd64 at 1600:
 # 256-key chunks over a 1200-key prefix; at 11300: 4-wave workgroups and
-# 128-key chunks; many_kv at 6000: 768-key chunks, two register sets.
+# 128-key chunks; many_kv at 6000 with a 2000-key prefix: 4-wave 128-key
+# chunks for the 4-row window, two 1280-key chunks of five steps per wave
+# for the 9-node tree; mha_hd128 at 70000: 768-key chunks of three steps
+# per wave with nontemporal key and value loads (one query tile).
 @pytest.mark.parametrize("name,L,k,cap", [("ragged_bf16", 45, 5, None), ("ragged_f32", 37, 4, None),
                                           ("gqa_hd64", 1200, 3, 1600), ("gqa_hd64", 1200, 3, 11300),
-                                          ("many_kv", 1000, 3, 6000), ("o_ring_hd128", 300, 10, None)])
+                                          ("many_kv", 2000, 3, 6000), ("mha_hd128", 2000, 5, 70000),
+                                          ("o_ring_hd128", 300, 10, None)])
 def test_poisoned_dead_rows_do_not_reach_logits(name, L, k, cap):
     shape = S.SHAPES[name]
     cap = cap or L + 2 * (k + 1) + 40

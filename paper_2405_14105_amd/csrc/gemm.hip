@@ -831,41 +831,49 @@ __global__ __launch_bounds__(kRingWaves * 64) void k_gemm_ring(GemmArgs a) {
 }
 
 // n-blocks per workgroup of each role's ring layout: the O projection one
-// (256 workgroups at d = 4096), QKV two (192 at the 8B shape), gate/up
-// seven (one workgroup per CU for 1792 n-blocks), the down projection four
-// with its K split (as the packed launch), the LM head eight
+// (256 workgroups at d = 4096), QKV two (192 at the 8B shape; one when one
+// round of single-n-block workgroups covers every n-block, e.g. 192 at the
+// 1B shape: 0.826 -> 0.811 ms per step, where two would leave 96
+// workgroups; at the 8B shape one is far slower, 18.4 vs 13.7 us, as every
+// CU then takes in twice the activation bytes), gate/up seven (one
+// workgroup per CU for 1792 n-blocks), the down projection four with its K
+// split (as the packed launch), the LM head eight
 template <int EPI>
 struct RingRole;
 template <>
 struct RingRole<EPI_QKV> {
   static constexpr int NBW = 2;
+  static int nbw(int Nb) { return Nb <= 256 ? 1 : 2; }
 };
 template <>
 struct RingRole<EPI_RESID> {
   static constexpr int NBW = 1;
+  static int nbw(int) { return NBW; }
 };
 template <>
 struct RingRole<EPI_SILU> {
   static constexpr int NBW = 7;
+  static int nbw(int) { return NBW; }
 };
 template <>
 struct RingRole<EPI_PART> {
   static constexpr int NBW = 4;
+  static int nbw(int) { return NBW; }
 };
 template <>
 struct RingRole<EPI_PARTRES> : RingRole<EPI_PART> {};
 template <>
 struct RingRole<EPI_STORE> {   // the LM head: many rounds of workgroups
   static constexpr int NBW = 8;
+  static int nbw(int) { return NBW; }
 };
 
 // k-blocks per wave the ring kernel is built for (a shape's k-range per wave
 // is rounded up to one of them; the extra tiles are zero)
 constexpr int kRingNk[] = {1, 2, 4, 8, 14, 16};
 
-template <int EPI, int NK, int MT>
+template <int EPI, int NBW, int NK, int MT>
 hipError_t launch_ring_nk(const GemmArgs& a, hipStream_t s) {
-  constexpr int NBW = RingRole<EPI>::NBW;
   if constexpr (NK * NBW < kRingDepth) {
     return hipErrorInvalidValue;
   } else {
@@ -875,28 +883,38 @@ hipError_t launch_ring_nk(const GemmArgs& a, hipStream_t s) {
   }
 }
 
-template <int EPI, int MT>
+template <int EPI, int NBW, int MT>
 hipError_t launch_ring_mt(const GemmArgs& a, hipStream_t s) {
   switch (a.ring_nk) {
-    case 1: return launch_ring_nk<EPI, 1, MT>(a, s);
-    case 2: return launch_ring_nk<EPI, 2, MT>(a, s);
-    case 4: return launch_ring_nk<EPI, 4, MT>(a, s);
-    case 8: return launch_ring_nk<EPI, 8, MT>(a, s);
-    case 14: return launch_ring_nk<EPI, 14, MT>(a, s);
-    case 16: return launch_ring_nk<EPI, 16, MT>(a, s);
+    case 1: return launch_ring_nk<EPI, NBW, 1, MT>(a, s);
+    case 2: return launch_ring_nk<EPI, NBW, 2, MT>(a, s);
+    case 4: return launch_ring_nk<EPI, NBW, 4, MT>(a, s);
+    case 8: return launch_ring_nk<EPI, NBW, 8, MT>(a, s);
+    case 14: return launch_ring_nk<EPI, NBW, 14, MT>(a, s);
+    case 16: return launch_ring_nk<EPI, NBW, 16, MT>(a, s);
   }
   return hipErrorInvalidValue;
 }
 
-template <int EPI>
-hipError_t launch_ring(const GemmArgs& a, int mt, hipStream_t s) {
+template <int EPI, int NBW>
+hipError_t launch_ring_nbw(const GemmArgs& a, int mt, hipStream_t s) {
   switch (mt) {
-    case 1: return launch_ring_mt<EPI, 1>(a, s);
-    case 2: return launch_ring_mt<EPI, 2>(a, s);
-    case 3: return launch_ring_mt<EPI, 3>(a, s);
-    case 4: return launch_ring_mt<EPI, 4>(a, s);
+    case 1: return launch_ring_mt<EPI, NBW, 1>(a, s);
+    case 2: return launch_ring_mt<EPI, NBW, 2>(a, s);
+    case 3: return launch_ring_mt<EPI, NBW, 3>(a, s);
+    case 4: return launch_ring_mt<EPI, NBW, 4>(a, s);
   }
   return hipErrorInvalidValue;
+}
+
+// the layout's n-blocks per workgroup (a.ring_nbw) picks the kernel
+template <int EPI>
+hipError_t launch_ring(const GemmArgs& a, int mt, hipStream_t s) {
+  if constexpr (EPI == EPI_QKV) {
+    if (a.ring_nbw == 1) return launch_ring_nbw<EPI, 1>(a, mt, s);
+  }
+  if (a.ring_nbw != RingRole<EPI>::NBW) return hipErrorInvalidValue;
+  return launch_ring_nbw<EPI, RingRole<EPI>::NBW>(a, mt, s);
 }
 
 // ring layout from the packed layout: one thread per 16 bytes of a tile
@@ -1051,12 +1069,12 @@ bool ring_config(int wtype, int epi_kind, int Nb, int Kb, int S, RingCfg* out) {
   if (wtype != W_BF16 || Nb < 1 || Kb < 1 || S < 1) return false;
   int nbw = 0;
   switch (epi_kind) {
-    case EPI_QKV: nbw = RingRole<EPI_QKV>::NBW; break;
-    case EPI_RESID: nbw = RingRole<EPI_RESID>::NBW; break;
-    case EPI_SILU: nbw = RingRole<EPI_SILU>::NBW; break;
+    case EPI_QKV: nbw = RingRole<EPI_QKV>::nbw(Nb); break;
+    case EPI_RESID: nbw = RingRole<EPI_RESID>::nbw(Nb); break;
+    case EPI_SILU: nbw = RingRole<EPI_SILU>::nbw(Nb); break;
     case EPI_PART:
-    case EPI_PARTRES: nbw = RingRole<EPI_PART>::NBW; break;
-    case EPI_STORE: nbw = RingRole<EPI_STORE>::NBW; break;
+    case EPI_PARTRES: nbw = RingRole<EPI_PART>::nbw(Nb); break;
+    case EPI_STORE: nbw = RingRole<EPI_STORE>::nbw(Nb); break;
     default: return false;
   }
   if (S > 1 && epi_kind != EPI_PART && epi_kind != EPI_PARTRES) return false;

@@ -123,6 +123,7 @@ struct GemmArgs {
   // RingCfg; one-row-tile launches that set it run the ring kernel.
   const void* Ws = nullptr;
   int ring_nk = 0;      // k-blocks per wave of that layout
+  int ring_nbw = 0;     // n-blocks per workgroup of that layout
   const void* Xhi;
   const void* Xlo;
   int Nb, Kb, M;

@@ -240,6 +240,7 @@ void set_ring(GemmArgs& g, const RingCfg& c, const void* ws, bool ring) {
   if (ring && c.nbw && ws) {
     g.Ws = ws;
     g.ring_nk = c.nk;
+    g.ring_nbw = c.nbw;
   }
 }
 
@@ -327,6 +328,7 @@ GemmArgs down_args(dsi_model* m, int l, int M, int mt, float* hidden_next = null
   if (g.Ws && g.S != m->rc_down.S) {   // the ring layout was built for another split
     g.Ws = nullptr;
     g.ring_nk = 0;
+    g.ring_nbw = 0;
   }
   g.epi.kind = EPI_PART;
   g.epi.out = m->delta;

@@ -105,6 +105,9 @@ SHAPES = {
     # at the full shapes
     "o_ring_hd64": Shape("o_ring_hd64", 2, 256, 32, 8, 64, 688, 2050, gains="random"),
     "o_ring_hd128": Shape("o_ring_hd128", 2, 256, 32, 8, 128, 344, 1003, gains="random"),
+    # a wide FFN on a small residual stream: 1125 gate/up n-blocks in 161
+    # ring workgroups of seven, and a four-way K split of the down projection
+    "ring_wide_ff": Shape("ring_wide_ff", 2, 256, 8, 2, 64, 9000, 1500, gains="random"),
     # drafters: small models sharing a target's vocabulary
     "tiny_draft": Shape("tiny_draft", 1, 64, 2, 2, 32, 128, 1024, wdtype="f32", kvdtype="f32"),
     "ragged_draft": Shape("ragged_draft", 1, 96, 3, 1, 32, 200, 1003, gains="random"),

@@ -43,6 +43,9 @@ CASES = [
     # projection runs on its ring layout; 700 keys span three key chunks
     ("o_ring_hd64", 700, 5),
     ("o_ring_hd128", 300, 10),
+    # a 9000-wide FFN: 161 gate/up ring workgroups, and the down projection
+    # split four ways (the small shapes above split it at most twice)
+    ("ring_wide_ff", 200, 6),
 ]
 
 

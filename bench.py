@@ -216,7 +216,26 @@ def run_gpu(args, wl):
     dsi.dsi_kv_destroy(kv)
     dsi.dsi_model_destroy(model)
     return {"ms": ms, "per_step": per, "kernels": kt, "n_accepted": n_acc.tolist(),
-            "host_us_per_call": enqueue / args.steps * 1e6, "copy_GBs": stream_copy_GBs(torch, dev)}
+            "host_us_per_call": enqueue / args.steps * 1e6, "copy_GBs": stream_copy_GBs(torch, dev),
+            "read": stream_read_GBs(dsi, torch, dev)}
+
+
+def stream_read_GBs(dsi, torch, dev, slice_bytes=640 << 20, slices=4, rounds=20):
+    """The library's streaming read (dsi_profile_stream) over four rotating
+    640 MiB slices -- more than the Infinity Cache holds, so every launch
+    reads HBM -- with plain and with nontemporal loads: bytes read per
+    second."""
+    buf = torch.empty(slice_bytes * slices, dtype=torch.uint8, device=dev)
+    buf.fill_(1)
+    sink = torch.zeros(16, dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+    out = {}
+    for name, nt in (("plain_GBs", False), ("nontemporal_GBs", True)):
+        nb, ms = dsi.dsi_profile_stream(buf, slice_bytes * slices, slices, nt, rounds, sink)
+        out[name] = round(nb / (ms * 1e-3) / 1e9, 1)
+    out["bytes_per_launch"] = nb
+    del buf, sink
+    return out
 
 
 def stream_copy_GBs(torch, dev, nbytes=1 << 30, reps=5):
@@ -614,6 +633,8 @@ def main():
                      "frac_of_peak": round(step_gbs / HBM_PEAK_GBS, 4)},
         "stream_copy": {"GBs": round(g["copy_GBs"], 1), "bytes": 2 << 30,
                         "step_frac_of_copy": round(sb["total"] / (ms * 1e-3) / 1e9 / g["copy_GBs"], 4)},
+        "stream_read": dict(g["read"], step_frac_of_nontemporal=round(
+            sb["total"] / (ms * 1e-3) / 1e9 / g["read"]["nontemporal_GBs"], 4)),
         "kernels_ms_per_step": {n: round(v["ms_per_step"], 4) for n, v in g["kernels"].items()},
         "gemm_isolated": {n: {"us": round(v["isolated_avg_ms"] * 1e3, 2),
                               "GBs": round(gb[n] / (v["isolated_avg_ms"] * 1e-3) / 1e9, 1)}

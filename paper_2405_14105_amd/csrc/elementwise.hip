@@ -242,6 +242,33 @@ __global__ void k_kv_poison(T* kc, T* vc, size_t layer_stride, int n_kv, int hd,
   }
 }
 
+// Streaming read rate (diagnostics): each wave reads a contiguous run of
+// per_wave_vec 16-byte vectors, 8 loads of 1 KB in flight (a ring, as the
+// GEMM weight streams), nontemporal when NT.  The XOR of the data is stored
+// only if it equals a fixed pattern, which keeps every load.
+template <int NT>
+__global__ __launch_bounds__(512) void k_stream_read(const u32x4* __restrict__ buf, size_t per_wave_vec,
+                                                     u32x4* sink) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const u32x4* p = buf + ((size_t)blockIdx.x * 8 + w) * per_wave_vec + lane;
+  const size_t iters = per_wave_vec / (8 * 64);
+  u32x4 acc = {0u, 0u, 0u, 0u};
+  u32x4 ring[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) ring[i] = NT ? __builtin_nontemporal_load(p + i * 64) : p[i * 64];
+  for (size_t it = 1; it < iters; ++it) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      acc ^= ring[i];
+      const u32x4* q = p + (it * 8 + i) * 64;
+      ring[i] = NT ? __builtin_nontemporal_load(q) : *q;
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 8; ++i) acc ^= ring[i];
+  if (acc.x == 0x9E3779B9u && acc.y == 0x7F4A7C15u && acc.z == 0x85EBCA6Bu && acc.w == 0xC2B2AE35u) *sink = acc;
+}
+
 __global__ void k_fill_zero(uint32_t* p, size_t n) {
   for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
     p[i] = 0u;
@@ -338,6 +365,16 @@ hipError_t launch_kv_poison(int kv_bf16, void* kc, void* vc, size_t layer_stride
   else
     hipLaunchKernelGGL(k_kv_poison<float>, grid, blk, 0, s, (float*)kc, (float*)vc, layer_stride, n_kv, hd,
                        maxlen, lens, window, std::numeric_limits<float>::quiet_NaN());
+  return hipGetLastError();
+}
+
+hipError_t launch_stream_read(const void* buf, size_t per_wave_vec, int nontemporal, void* sink, hipStream_t s) {
+  if (nontemporal)
+    hipLaunchKernelGGL(k_stream_read<1>, dim3(kStreamWorkgroups), dim3(512), 0, s, (const u32x4*)buf, per_wave_vec,
+                       (u32x4*)sink);
+  else
+    hipLaunchKernelGGL(k_stream_read<0>, dim3(kStreamWorkgroups), dim3(512), 0, s, (const u32x4*)buf, per_wave_vec,
+                       (u32x4*)sink);
   return hipGetLastError();
 }
 

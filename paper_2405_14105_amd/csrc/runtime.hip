@@ -1282,6 +1282,40 @@ dsi_status dsi_profile_end(dsi_model* m, int32_t* launches, double* total_ms) {
   return DSI_OK;
 }
 
+dsi_status dsi_profile_stream(const void* d_buf, uint64_t bytes, int32_t slices, int32_t nontemporal,
+                              int32_t rounds, void* d_sink, uint64_t* bytes_per_launch, double* avg_ms) {
+  if (!d_buf || !d_sink || !bytes_per_launch || !avg_ms || rounds < 1 || slices < 1)
+    return fail(DSI_EINVAL, "bad argument");
+  if (((uintptr_t)d_buf & 15) != 0) return fail(DSI_EINVAL, "buffer not 16-byte aligned");
+  const uint64_t slice = bytes / (uint64_t)slices;
+  const uint64_t waves = (uint64_t)kStreamWorkgroups * 8;
+  const uint64_t run = slice / waves / 8192 * 8192;   // bytes per wave: whole rings of 8 x 1 KB
+  if (run < 8192 || slice < (16ull << 20)) return fail(DSI_EINVAL, "slices must hold at least 16 MiB");
+  const size_t per_wave_vec = (size_t)(run / 16);
+  hipEvent_t e0, e1;
+  HIP_TRY(hipEventCreate(&e0));
+  HIP_TRY(hipEventCreate(&e1));
+  dsi_status st = DSI_OK;
+  auto go = [&](int r) -> hipError_t {
+    return launch_stream_read((const char*)d_buf + (size_t)(r % slices) * slice, per_wave_vec, nontemporal,
+                              d_sink, nullptr);
+  };
+  hipError_t e = go(0);   // warm-up
+  if (e == hipSuccess) e = hipEventRecord(e0, nullptr);
+  for (int r = 1; r <= rounds && e == hipSuccess; ++r) e = go(r);
+  if (e == hipSuccess) e = hipEventRecord(e1, nullptr);
+  if (e == hipSuccess) e = hipEventSynchronize(e1);
+  float ms = 0.f;
+  if (e == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
+  hipEventDestroy(e0);
+  hipEventDestroy(e1);
+  if (e != hipSuccess) st = fail(DSI_EHIP, "HIP error: %s", hipGetErrorString(e));
+  if (st != DSI_OK) return st;
+  *bytes_per_launch = run * waves;
+  *avg_ms = (double)ms / rounds;
+  return DSI_OK;
+}
+
 dsi_status dsi_profile_kernel(dsi_model* m, dsi_kv* kv, int32_t cls, int32_t rounds, int32_t* launches,
                               double* avg_ms) {
   if (!m || !kv || kv->m != m || !launches || !avg_ms || rounds < 1)

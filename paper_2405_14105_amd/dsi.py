@@ -28,7 +28,7 @@ EXPORTED = (
     "dsi_kv_destroy", "dsi_prefill", "dsi_verify", "dsi_verify_tree", "dsi_draft", "dsi_accept",
     "dsi_accept_noalloc",
     "dsi_kv_rollback", "dsi_kv_poison", "dsi_kv_length", "dsi_sync", "dsi_kv_export", "dsi_kv_import", "dsi_kv_set_length",
-    "dsi_profile_begin", "dsi_profile_end", "dsi_profile_kernel", "dsi_last_error",
+    "dsi_profile_begin", "dsi_profile_end", "dsi_profile_kernel", "dsi_profile_stream", "dsi_last_error",
 )
 DSI_K_QKV, DSI_K_ATTN, DSI_K_OPROJ, DSI_K_GATEUP, DSI_K_DOWN, DSI_K_HEAD, DSI_K_VERIFY = range(1, 8)
 
@@ -100,6 +100,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "dsi_profile_begin": ([P, I32], I32),
         "dsi_profile_end": ([P, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_double)], I32),
         "dsi_profile_kernel": ([P, P, I32, I32, ctypes.POINTER(ctypes.c_int32),
+                                ctypes.POINTER(ctypes.c_double)], I32),
+        "dsi_profile_stream": ([P, ctypes.c_uint64, I32, I32, I32, P, ctypes.POINTER(ctypes.c_uint64),
                                 ctypes.POINTER(ctypes.c_double)], I32),
         "dsi_last_error": ([], ctypes.c_char_p),
     }
@@ -242,6 +244,16 @@ def dsi_profile_kernel(model: int, kv: int, kernel_class: int, rounds: int = 3):
     t = ctypes.c_double()
     _check(load().dsi_profile_kernel(model, kv, kernel_class, rounds, ctypes.byref(n), ctypes.byref(t)))
     return n.value, t.value
+
+
+def dsi_profile_stream(d_buf, nbytes: int, slices: int, nontemporal: bool, rounds: int, d_sink):
+    """Returns (bytes per launch, avg_ms) of the library's streaming read over
+    `slices` slices of the device buffer d_buf, one per launch in turn."""
+    b = ctypes.c_uint64()
+    t = ctypes.c_double()
+    _check(load().dsi_profile_stream(_ptr(d_buf), nbytes, slices, int(bool(nontemporal)), rounds, _ptr(d_sink),
+                                     ctypes.byref(b), ctypes.byref(t)))
+    return b.value, t.value
 
 
 def dsi_last_error() -> str:

@@ -113,7 +113,10 @@ def test_prefill_last_logits(name):
 #     fp32 keys and values;
 #   mha_hd128, 1 x 70000: one query tile with several steps per wave, so the
 #     keys and values are streamed with nontemporal loads (768-key chunks,
-#     three chunks).
+#     three chunks);
+#   o_ring_hd128 (head dim 128) at 8000 and o_ring_hd64 at 12000 positions:
+#     three and four query tiles whose single key chunk takes four and six
+#     steps per wave (the kernel normalises its own output).
 @pytest.mark.parametrize("name,n_windows,max_len,win,L,k", [
     ("gqa_hd64", 1, 1600, 0, 1300, 5),
     ("ragged_bf16", 1, 1600, 0, 1100, 4),
@@ -123,6 +126,8 @@ def test_prefill_last_logits(name):
     ("tiny", 8, 2100, 3, 900, 5),
     ("tiny", 1, 33000, 0, 1500, 5),
     ("mha_hd128", 1, 70000, 0, 2000, 5),
+    ("o_ring_hd128", 1, 8000, 0, 1000, 10),
+    ("o_ring_hd64", 1, 12000, 0, 1000, 15),
 ])
 def test_multichunk_attention(name, n_windows, max_len, win, L, k):
     shape = S.SHAPES[name]

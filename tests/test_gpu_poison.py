@@ -28,10 +28,13 @@ SEED = 0
 # 128-key chunks; many_kv at 6000 with a 2000-key prefix: 4-wave 128-key
 # chunks for the 4-row window, two 1280-key chunks of five steps per wave
 # for the 9-node tree; mha_hd128 at 70000: 768-key chunks of three steps
-# per wave with nontemporal key and value loads (one query tile).
+# per wave with nontemporal key and value loads (one query tile);
+# o_ring_hd128 at 8000 with k 10: three query tiles in one 1024-key chunk
+# of four steps per wave.
 @pytest.mark.parametrize("name,L,k,cap", [("ragged_bf16", 45, 5, None), ("ragged_f32", 37, 4, None),
                                           ("gqa_hd64", 1200, 3, 1600), ("gqa_hd64", 1200, 3, 11300),
                                           ("many_kv", 2000, 3, 6000), ("mha_hd128", 2000, 5, 70000),
+                                          ("o_ring_hd128", 1000, 10, 8000),
                                           ("o_ring_hd128", 300, 10, None)])
 def test_poisoned_dead_rows_do_not_reach_logits(name, L, k, cap):
     shape = S.SHAPES[name]

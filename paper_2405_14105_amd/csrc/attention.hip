@@ -10,16 +10,16 @@
 // into tiles of 16 queries.  Per 32-key step a wavefront computes
 //   S^T[key][query] = K . Q^T     (A = 16 K rows, B = Q^T hi/lo)
 //   O^T[d][query]  += V^T . P^T   (A = V^T rows)
-// on the cache's 32-position blocks (kc_off / vc_off): the keys and the
-// values of one step are each one contiguous block (8 KB at hd = 128) and
-// every fragment load reads whole 128-byte lines
 // with 16x16x32 bf16 MFMAs (two per product for the hi/lo query or
 // probability split), so every operand is a 16-byte lane load and the
 // query owned by a lane (l % 16) is the same in S^T, P^T and O^T: the
 // online-softmax rescale is lane-local.  The K rows of the two S^T tiles are
 // permuted so that lane l ends up holding keys p0 + 8*(l/16) + 0..7, which is
 // exactly its P^T B-operand fragment.  fp32 caches use 16x16x4 fp32 MFMAs
-// on the same data arrangement.
+// on the same data arrangement.  The cache is stored in 32-position blocks
+// (kc_off / vc_off): the keys and the values of one step are each one
+// contiguous block (8 KB at hd = 128) and every fragment load reads whole
+// 128-byte lines.
 #include <math.h>
 
 #include "device_util.h"

@@ -33,7 +33,7 @@ METRIC = "verify-step latency (ms) + verified draft tokens/s, 8B-shape k=10; % H
 # scales from a 512 MiB copy).  Reported only while the GEMM sources are the
 # ones the counters were taken with.
 TRAFFIC_MEASURED = {"workload": "llama8b_L2048_k10", "bytes": 237.88e6,
-                    "sources_sha256": "b47dbfaddaa6da67930c36d93646ea43f98880ddad44cc1f99cb80a53c0cf564"}
+                    "sources_sha256": "22b0e5bb711ea6454e590340fa63b3fc9586bd2e92dc7a86303b7f929fc42944"}
 GEMM_SOURCES = ("paper_2405_14105_amd/csrc/gemm.hip", "paper_2405_14105_amd/csrc/device_util.h",
                 "paper_2405_14105_amd/csrc/internal.h")
 HBM_PEAK_GBS = 8000.0

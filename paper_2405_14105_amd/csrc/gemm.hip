@@ -684,7 +684,8 @@ constexpr int ring_red_nb(int nbw, int mt) { return 16 / mt < nbw ? 16 / mt : nb
 
 // RMSNorm sums of rows w and w + kRingWaves (the first 16 rows), requested
 // before the weights and reduced after the main loop; rows beyond 16 (wave
-// w: rows w + 8h) are loaded after it
+// w: rows w + 8h) are loaded after it, all at once (42-row batch: step 4.65
+// -> 4.62 ms against one conditional load after another)
 struct RingSsq {
   float v[2][kSsqPer];
 };
@@ -718,6 +719,16 @@ __device__ __forceinline__ RingSsq ring_ssq_prefetch(const GemmArgs& a) {
 template <int MT>
 __device__ __forceinline__ void ring_row_scales(const GemmArgs& a, const RingSsq& pre, float* rs) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  // rows past the first 16: every load issued at once (indices clamped into
+  // the buffer, invalid entries zeroed after), one wait for all of them
+  constexpr int HL = 2 * MT - 2 > 0 ? 2 * MT - 2 : 1;
+  float late[HL][kSsqPer];
+#pragma unroll
+  for (int h = 2; h < 2 * MT; ++h) {
+    const int m = min(w + h * kRingWaves, a.M - 1);
+#pragma unroll
+    for (int c = 0; c < kSsqPer; ++c) late[h - 2][c] = a.ssq[(size_t)m * a.ssq_n + min(lane + 64 * c, a.ssq_n - 1)];
+  }
 #pragma unroll
   for (int h = 0; h < 2 * MT; ++h) {
     const int m = w + h * kRingWaves;
@@ -727,8 +738,7 @@ __device__ __forceinline__ void ring_row_scales(const GemmArgs& a, const RingSsq
       if (h < 2) {
         v[c] = pre.v[h < 2 ? h : 0][c];
       } else {
-        v[c] = 0.f;
-        if (m < a.M && lane + 64 * c < a.ssq_n) v[c] = a.ssq[(size_t)m * a.ssq_n + lane + 64 * c];
+        v[c] = (m < a.M && lane + 64 * c < a.ssq_n) ? late[h < 2 ? 0 : h - 2][c] : 0.f;
       }
     }
     float sum = 0.f;

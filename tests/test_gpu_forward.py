@@ -171,10 +171,15 @@ def test_empty_prefix_and_k0():
 # prefix, where the 40-key window's later chunks hold no key at all (their
 # partials carry max -inf and sum 0) and alone it takes the single-chunk
 # path that normalises inside the attention kernel
-@pytest.mark.parametrize("lens,cap", [([20, 33, 47, 5], 64), ([300, 1250, 40], 1600)])
-def test_batched_windows_ragged_and_batch_invariant(lens, cap):
-    shape = S.SHAPES["gqa_hd64"]
-    k = 4
+# ... and with three and four row tiles (48 and 64 rows: four windows of 12
+# and of 16 rows), where every GEMM role runs its several-row-tile ring
+# kernel: still bit-identical to each window alone.
+@pytest.mark.parametrize("name,lens,cap,k", [("gqa_hd64", [20, 33, 47, 5], 64, 4),
+                                             ("gqa_hd64", [300, 1250, 40], 1600, 4),
+                                             ("gqa_hd64", [20, 33, 47, 5], 80, 11),
+                                             ("o_ring_hd128", [40, 70, 25, 55], 100, 15)])
+def test_batched_windows_ragged_and_batch_invariant(name, lens, cap, k):
+    shape = S.SHAPES[name]
     B = len(lens)
     with Rig(shape, SEED, B, cap) as rig:
         prefixes = [S.prefix_tokens(shape, SEED, b, lens[b]) for b in range(B)]

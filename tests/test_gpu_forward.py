@@ -205,6 +205,36 @@ def test_batched_windows_ragged_and_batch_invariant(name, lens, cap, k):
             assert rig.length(b) == lens[b] + res["n"][b] + 1
 
 
+# Models created with DSI_RING=0 keep only the packed weight layout, so every
+# GEMM runs the packed kernels (k_gemm_bf16: the two-set pipelined loop for
+# one to three row tiles of QKV, O and gate/up, the batch loop otherwise) --
+# the path of shapes without a ring layout (the 13B shape).  One, three and
+# four row tiles, each window checked against the oracle and against itself
+# verified alone.
+@pytest.mark.parametrize("name,lens,k", [("o_ring_hd64", [300], 10), ("gqa_hd64", [20, 33, 47, 5], 11),
+                                         ("o_ring_hd128", [40, 70, 25, 55], 15)])
+def test_packed_kernels_without_ring(monkeypatch, name, lens, k):
+    monkeypatch.setenv("DSI_RING", "0")
+    shape = S.SHAPES[name]
+    B = len(lens)
+    with Rig(shape, SEED, B, max(lens) + k + 30) as rig:
+        prefixes = [S.prefix_tokens(shape, SEED, b, lens[b]) for b in range(B)]
+        for b in range(B):
+            rig.prefill(b, prefixes[b])
+        wi = S.window_inputs(shape, SEED, B, k)
+        out = rig.verify(0, wi["tokens"], wi["q"], wi["u"], commit=False)
+        zz = out["logits"].reshape(B, k + 1, shape.vocab)
+        for b in range(B):
+            zo = oracle_logits(shape, prefixes[b], wi["tokens"][b])
+            delta = float(np.abs(zz[b] - zo).max())
+            print(f"{name} packed, window {b}: max|dz| = {delta:.3g}")
+            assert delta <= TOL["bf16"] and delta <= reg_of(shape), (b, delta)
+            split_check(zz[b], wi["tokens"][b], wi["q"][b], wi["u"][b], out["n"][b], out["token"][b])
+            if B > 1:
+                one = rig.verify(b, wi["tokens"][b:b + 1], wi["q"][b:b + 1], wi["u"][b:b + 1], commit=False)
+                assert np.array_equal(one["logits"], zz[b])
+
+
 def test_rollback_then_reverify_is_bit_identical():
     shape = S.SHAPES["ragged_bf16"]
     L, k = 30, 5

@@ -64,10 +64,13 @@ def run(rig, buf, window0, B, k, mode, commit):
 # launch and the combine inside the graph, the longest window 1010 keys so
 # that commits take its key range past 1024 (a fifth chunk: a new plan and
 # a new graph) between replays
-@pytest.mark.parametrize("name,lens,cap", [("ragged_bf16", [17, 40, 29], 200),
-                                           ("gqa_hd64", [17, 40, 29], 200),
-                                           ("gqa_hd64", [300, 1010, 250], 1600)])
-def test_graph_replays_match_eager(name, lens, cap):
+# ... and o_ring_hd128 with 16-row windows: the three windows together run
+# the three-row-tile kernels (48 rows), one window alone the one-row-tile ones
+@pytest.mark.parametrize("name,lens,cap,kbig", [("ragged_bf16", [17, 40, 29], 200, 4),
+                                                ("gqa_hd64", [17, 40, 29], 200, 4),
+                                                ("gqa_hd64", [300, 1010, 250], 1600, 4),
+                                                ("o_ring_hd128", [40, 70, 25], 300, 15)])
+def test_graph_replays_match_eager(name, lens, cap, kbig):
     shape = S.SHAPES[name]
     B = len(lens)
     side = torch.cuda.Stream()
@@ -84,7 +87,7 @@ def test_graph_replays_match_eager(name, lens, cap):
             # same shapes repeatedly (replays), interleaved with other shapes,
             # greedy mode, single windows, commits and rollbacks
             for it in range(14):
-                k = (4, 4, 4, 2, 4, 4, 2, 4, 4, 4, 4, 2, 4, 4)[it]
+                k = (kbig, kbig, kbig, 2, kbig, kbig, 2, kbig, kbig, kbig, kbig, 2, kbig, kbig)[it]
                 mode = dsi.DSI_GREEDY if it in (5, 9) else dsi.DSI_SAMPLE
                 w0, nb = (1, 1) if it in (6, 11) else (0, B)
                 schedule.append((k, mode, w0, nb, it % 3 != 2))

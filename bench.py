@@ -34,6 +34,12 @@ METRIC = "verify-step latency (ms) + verified draft tokens/s, 8B-shape k=10; % H
 # ones the counters were taken with.
 TRAFFIC_MEASURED = {"workload": "llama8b_L2048_k10", "bytes": 237.88e6,
                     "sources_sha256": "22b0e5bb711ea6454e590340fa63b3fc9586bd2e92dc7a86303b7f929fc42944"}
+# Matrix-core work of the same kernel from the counter run in
+# profiles/verify_8b_mfma_counters.md: SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 flops
+# per launch (what the MFMAs execute: 16-row tiles, both hi/lo halves) and
+# SQ_VALU_MFMA_BUSY_CYCLES against all SIMD cycles.  Same source condition.
+MFMA_MEASURED = {"workload": "llama8b_L2048_k10", "gflop_per_launch": 7.52, "busy_pct": 6.9,
+                 "sources_sha256": TRAFFIC_MEASURED["sources_sha256"]}
 GEMM_SOURCES = ("paper_2405_14105_amd/csrc/gemm.hip", "paper_2405_14105_amd/csrc/device_util.h",
                 "paper_2405_14105_amd/csrc/internal.h")
 HBM_PEAK_GBS = 8000.0
@@ -89,15 +95,30 @@ def gemm_bytes(shape, M) -> dict:
             "head": b(s.vocab, d, s.vocab * 4)}
 
 
-def measured_traffic(workload: str):
+def gemm_sources_sha256() -> str:
     import hashlib
     h = hashlib.sha256()
     for f in GEMM_SOURCES:
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(fh.read())
-    if workload == TRAFFIC_MEASURED["workload"] and h.hexdigest() == TRAFFIC_MEASURED["sources_sha256"]:
+    return h.hexdigest()
+
+
+def measured_traffic(workload: str):
+    if workload == TRAFFIC_MEASURED["workload"] and gemm_sources_sha256() == TRAFFIC_MEASURED["sources_sha256"]:
         return TRAFFIC_MEASURED["bytes"]
     return None
+
+
+def measured_mfma(workload: str, avg_launch_ms: float):
+    """Counter-measured matrix-core use of the gate/up launch, with its rate
+    at the live launch duration; None unless the sources are the measured
+    ones."""
+    if workload != MFMA_MEASURED["workload"] or gemm_sources_sha256() != MFMA_MEASURED["sources_sha256"]:
+        return None
+    tflops = MFMA_MEASURED["gflop_per_launch"] / (avg_launch_ms * 1e-3) / 1e3
+    return {"gflop_per_launch": MFMA_MEASURED["gflop_per_launch"], "TFLOPs": round(tflops, 1),
+            "frac_of_bf16_peak": round(tflops / 2500.0, 4), "busy_pct": MFMA_MEASURED["busy_pct"]}
 
 
 # ------------------------------------------------------------------ GPU part
@@ -594,6 +615,7 @@ def main():
     roof = {"bound": "hbm", "kernel": "gate/up projection + SwiGLU (k_gemm_ring, EPI_SILU)",
             "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(wl.name),
+            "mfma": measured_mfma(wl.name, gu["isolated_avg_ms"]),
             "bytes_per_launch": gu_bytes, "avg_launch_ms": round(gu["isolated_avg_ms"], 5),
             "avg_launch_ms_in_step": round(gu["avg_ms"], 5),
             "timing": ("HIP events around every layer's gate/up launch replayed back to back "

@@ -81,6 +81,7 @@ __global__ __launch_bounds__(NWV * 64, (NWV == 4 && KVB) ? 3 : 1) void k_attn(At
   const size_t vbase = ((size_t)wabs * a.n_kv + kvh) * (size_t)HD * a.maxlen;
   const int r16 = lane & 15;
   const int kgrp = (lane >> 4) * 8;
+  const float scale2 = a.scale * 1.44269504088896340736f;   // log2 e
 
   // K and V of one 32-key step
   struct KV16 {
@@ -191,44 +192,58 @@ __global__ __launch_bounds__(NWV * 64, (NWV == 4 && KVB) ? 3 : 1) void k_attn(At
       }
     }
     if (pnext >= 0 && pnext < c1) load_k_into(d16, d32, pnext);
-    // lane holds keys p0 + kgrp + (t*4 + j) for query (lane & 15)
+    // Lane holds keys p0 + kgrp + (t*4 + j) for query (lane & 15).  Scores
+    // are kept in base-2 units (scale times log2 e), so that each
+    // exponential is one v_exp_f32.  A step whose keys are all live keys of
+    // the chunk that every query row sees -- prefix keys (rows sit at
+    // positions len and later; a tree row sees the keys before len only) --
+    // needs no mask, a test that is the same for the whole wave.
+    const bool full = p0 + 32 <= c1 && p0 + 32 <= (TREE ? len : len + 1);
     float sv[8];
     float mloc = -INFINITY;
+    if (full) {
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+      for (int e = 0; e < 8; ++e) {
+        sv[e] = st[e >> 2][e & 3] * scale2;
+        mloc = fmaxf(mloc, sv[e]);
+      }
+    } else {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int key = p0 + kgrp + t * 4 + j;
-        const float v = st[t][j] * a.scale;
+      for (int e = 0; e < 8; ++e) {
+        const int key = p0 + kgrp + e;
         bool vis = key <= qpos && key < c1;
         if constexpr (TREE) vis = vis && (key < len || ((anc >> ((key - len) & 63)) & 1ull));
-        const float vm = vis ? v : -INFINITY;
-        sv[t * 4 + j] = vm;
-        mloc = fmaxf(mloc, vm);
+        sv[e] = vis ? st[e >> 2][e & 3] * scale2 : -INFINITY;
+        mloc = fmaxf(mloc, sv[e]);
       }
+    }
     mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
     mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
     const float mnew = fmaxf(mrun, mloc);
     const float base = (mnew == -INFINITY) ? 0.f : mnew;
-    const float alpha = expf(mrun - base);
     float pv[8];
     float lsum = 0.f;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      pv[e] = expf(sv[e] - base);
+      pv[e] = __builtin_amdgcn_exp2f(sv[e] - base);
       lsum += pv[e];
     }
-    lrun = lrun * alpha + lsum;
-    mrun = mnew;
+    // rescale only when some row's running maximum moved (else alpha is 1)
+    if (__ballot(mnew != mrun)) {
+      const float alpha = __builtin_amdgcn_exp2f(mrun - base);
+      lrun *= alpha;
 #pragma unroll
-    for (int t = 0; t < DT; ++t) o[t] *= alpha;
+      for (int t = 0; t < DT; ++t) o[t] *= alpha;
+    }
+    lrun += lsum;
+    mrun = mnew;
 
     // keys at or past c1 (past the window's rows: dead cache rows or beyond
     // the allocation) have probability 0, but 0 * NaN is not 0: their V
     // elements are zeroed, so that whatever a dead row holds never reaches
     // the output (dsi_kv_poison)
     const int nv = c1 - (p0 + kgrp);   // valid keys among the lane's 8
-    if (nv < 8) {
+    if (!full && nv < 8) {
       if (KVB) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
@@ -306,7 +321,7 @@ __global__ __launch_bounds__(NWV * 64, (NWV == 4 && KVB) ? 3 : 1) void k_attn(At
       float L = 0.f;
 #pragma unroll
       for (int ww = 0; ww < NWV; ++ww) {
-        const float f = expf(sm[ww][q] - b);
+        const float f = __builtin_amdgcn_exp2f(sm[ww][q] - b);
         acc += so[ww][t][l] * f;
         L += sl[ww][q] * f;
       }
@@ -326,7 +341,7 @@ __global__ __launch_bounds__(NWV * 64, (NWV == 4 && KVB) ? 3 : 1) void k_attn(At
     const float b = (M == -INFINITY) ? 0.f : M;
     f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int ww = 0; ww < NWV; ++ww) acc += so[ww][t][l] * expf(sm[ww][q] - b);
+    for (int ww = 0; ww < NWV; ++ww) acc += so[ww][t][l] * __builtin_amdgcn_exp2f(sm[ww][q] - b);
     float* dst = a.part_o + (zyc * 16 + q) * HD + t * 16 + (l >> 4) * 4;
     *(float4*)dst = float4{acc[0], acc[1], acc[2], acc[3]};
   }
@@ -338,8 +353,8 @@ __global__ __launch_bounds__(NWV * 64, (NWV == 4 && KVB) ? 3 : 1) void k_attn(At
     const float b = (M == -INFINITY) ? 0.f : M;
     float L = 0.f;
 #pragma unroll
-    for (int ww = 0; ww < NWV; ++ww) L += sl[ww][q] * expf(sm[ww][q] - b);
-    a.part_ml[zyc * 16 + q] = make_float2(M, L);
+    for (int ww = 0; ww < NWV; ++ww) L += sl[ww][q] * __builtin_amdgcn_exp2f(sm[ww][q] - b);
+    a.part_ml[zyc * 16 + q] = make_float2(M * 0.69314718055994530942f, L);   // back to natural units
   }
 
 }

@@ -114,9 +114,16 @@ def test_prefill_last_logits(name):
 #   mha_hd128, 1 x 70000: one query tile with several steps per wave, so the
 #     keys and values are streamed with nontemporal loads (768-key chunks,
 #     three chunks);
-#   o_ring_hd128 (head dim 128) at 8000 and o_ring_hd64 at 12000 positions:
-#     three and four query tiles whose single key chunk takes four and six
-#     steps per wave (the kernel normalises its own output).
+#   o_ring_hd128 (head dim 128) at 8000 positions with k 10: three query
+#     tiles whose single 1024-key chunk takes four steps per wave (the
+#     kernel normalises its own output); with a 200-key prefix (one partial
+#     step, a wave with no key at all); on window 1 of a three-window cache;
+#   o_ring_hd64 at 12000 positions: two query tiles (k 7: 768-key chunks of
+#     three steps per wave, the prefix spilling into a second chunk) and
+#     four (k 15, whose single chunk takes six steps per wave);
+#   o_ring_hd128 (k 10) and o_ring_hd64 (k 7) at 30000 positions with a
+#     2300-key prefix: up to ten and eight steps per wave (3072- and
+#     2048-key chunks) over mostly mask-free prefix steps.
 @pytest.mark.parametrize("name,n_windows,max_len,win,L,k", [
     ("gqa_hd64", 1, 1600, 0, 1300, 5),
     ("ragged_bf16", 1, 1600, 0, 1100, 4),
@@ -127,7 +134,12 @@ def test_prefill_last_logits(name):
     ("tiny", 1, 33000, 0, 1500, 5),
     ("mha_hd128", 1, 70000, 0, 2000, 5),
     ("o_ring_hd128", 1, 8000, 0, 1000, 10),
+    ("o_ring_hd128", 1, 8000, 0, 200, 10),
+    ("o_ring_hd128", 3, 8000, 1, 1000, 10),
+    ("o_ring_hd64", 1, 12000, 0, 1000, 7),
     ("o_ring_hd64", 1, 12000, 0, 1000, 15),
+    ("o_ring_hd128", 1, 30000, 0, 2300, 10),
+    ("o_ring_hd64", 1, 30000, 0, 2300, 7),
 ])
 def test_multichunk_attention(name, n_windows, max_len, win, L, k):
     shape = S.SHAPES[name]

@@ -414,6 +414,21 @@ dsi_status plan_attention(dsi_model* m, dsi_kv* kv, int window0, int B, int R, A
   const long long full8 = (long long)kv->n_windows * m->hkv * p->n_qtiles * cdiv(kv->max_len, chunk8);
   p->waves = (chunk8 == q8 && full8 > 256) ? 4 : kAttnWaves;
   p->chunk = p->waves == 4 ? chunk_of(2 * want, 4 * 32) : chunk_of(want, q8);
+  // A short cache is read in one chunk per (window, KV head, query tile):
+  // the kernel then normalises its own output and the combine launch (~4-5
+  // us) is saved, at the price of a few dependent steps per wave -- up to
+  // three, or five when there are at least 64 such workgroups (many
+  // windows).  Measured per step: 1B at 518 positions 0.797 -> 0.771 ms,
+  // 8B at 523 3.243 -> 3.217 ms, the 7-window 8B batch at 1036 (112
+  // workgroups) 4.615 -> 4.545 ms; a single 8B or 13B window at 1035
+  // positions (five steps, 24 and 40 workgroups) was 2 % slower, at 2059
+  // (nine steps) 10 %.
+  const int steps1 = cdiv(kv->max_len, q8);
+  const long long wg1 = (long long)kv->n_windows * m->hkv * p->n_qtiles;
+  if (steps1 <= 3 || (steps1 <= 5 && wg1 >= 64)) {
+    p->waves = kAttnWaves;
+    p->chunk = chunk_of(1, q8);
+  }
   p->n_chunks = (int)((kmax + p->chunk - 1) / p->chunk);
   const size_t nparts = (size_t)B * m->hkv * p->n_qtiles * p->n_chunks * 16;
   DSI_TRY(ensure(m->attn_o, nparts * m->hd * sizeof(float)));

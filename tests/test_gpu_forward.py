@@ -40,7 +40,8 @@ CASES = [
     ("hd96_kvf32", 41, 5),
     ("f32w_bf16kv", 36, 4),
     # the 1B / 8B attention geometry on a small residual stream: the O
-    # projection runs on its ring layout; 700 keys span three key chunks
+    # projection runs on its ring layout; the 717-position cache is read in
+    # one key chunk of three steps per wave (no combine launch)
     ("o_ring_hd64", 700, 5),
     ("o_ring_hd128", 300, 10),
     # a 9000-wide FFN: 161 gate/up ring workgroups, and the down projection

@@ -187,13 +187,18 @@ def test_empty_prefix_and_k0():
 # ... and with three and four row tiles (48 and 64 rows: four windows of 12
 # and of 16 rows), where every GEMM role runs its several-row-tile ring
 # kernel, also with fp32 weights and cache (tiny) and bf16 weights over an
-# fp32 cache (hd96_kvf32): still bit-identical to each window alone.
+# fp32 cache (hd96_kvf32): still bit-identical to each window alone
+# ... and three 11-row windows of o_ring_hd128 over a 1200-position cache:
+# 72 (window, KV head, query tile) workgroups of five 32-key steps read the
+# cache in one key chunk each (no combine launch), as the 7-window 8B batch
+# does, with the three-row-tile GEMMs.
 @pytest.mark.parametrize("name,lens,cap,k", [("gqa_hd64", [20, 33, 47, 5], 64, 4),
                                              ("gqa_hd64", [300, 1250, 40], 1600, 4),
                                              ("gqa_hd64", [20, 33, 47, 5], 80, 11),
                                              ("o_ring_hd128", [40, 70, 25, 55], 100, 15),
                                              ("tiny", [30, 12, 50, 41], 80, 11),
-                                             ("hd96_kvf32", [25, 60, 33, 8], 90, 15)])
+                                             ("hd96_kvf32", [25, 60, 33, 8], 90, 15),
+                                             ("o_ring_hd128", [1000, 1100, 950], 1200, 10)])
 def test_batched_windows_ragged_and_batch_invariant(name, lens, cap, k):
     shape = S.SHAPES[name]
     B = len(lens)

@@ -70,11 +70,14 @@ def kv_close(rig, window, shape, cache, n_rows):
 # mask meets the chunk partials and their combine; with 11300 positions the
 # plan takes 4-wave workgroups and 128-key chunks (10 of them); many_kv with
 # 6000 positions and a 2000-key prefix: two chunks of 1280 or 1536 keys
-# (three or four query tiles), five or six steps per wave
+# (three or four query tiles), five or six steps per wave; gqa_hd64 with a
+# 500-key prefix and room for the tree only: one key chunk whose waves take
+# two or three pipelined steps under the tree mask, normalised in the kernel
 @pytest.mark.parametrize("name,L,cap", [("tiny", 40, None), ("ragged_bf16", 33, None),
                                         ("gqa_hd64", 70, None), ("hd96_kvf32", 30, None),
                                         ("f32w_bf16kv", 25, None), ("gqa_hd64", 1200, 1600),
-                                        ("gqa_hd64", 1200, 11300), ("many_kv", 2000, 6000)])
+                                        ("gqa_hd64", 1200, 11300), ("many_kv", 2000, 6000),
+                                        ("gqa_hd64", 500, None)])
 def test_tree_matches_oracle_and_commits(name, L, cap):
     shape = S.SHAPES[name]
     tol = tol_of(shape)

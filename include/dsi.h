@@ -328,16 +328,19 @@ dsi_status dsi_profile_kernel(dsi_model* m, dsi_kv* kv, int32_t kernel_class, in
  * aligned) as `slices` equal slices, one slice per launch in turn (slices
  * whose sum exceeds the 256 MB Infinity Cache make every launch read HBM),
  * `rounds` launches after one warm-up launch, between one pair of HIP events
- * on the null stream of the current device.  A launch has 256 workgroups of
- * 8 waves; each wave reads a contiguous run with 8 loads of 1 KB in flight,
- * nontemporal when `nontemporal` is nonzero.  d_sink: caller-owned device
- * memory of at least 16 bytes, written only if the data XORs to a fixed
- * pattern.  Returns the bytes one launch reads (each slice rounded down to
- * whole 8 KB runs per wave) and the average launch duration; synchronises.
- * DSI_EINVAL for null pointers, a misaligned buffer, rounds < 1, slices < 1
- * or slices of less than 16 MiB; DSI_EHIP if a launch or event fails. */
+ * on the null stream of the current device.  A launch has `workgroups`
+ * workgroups (0: 256, one per CU; at most 4096) of 8 waves; each wave reads
+ * a contiguous run with 8 loads of 1 KB in flight, nontemporal when
+ * `nontemporal` is nonzero.  d_sink: caller-owned device memory of at least
+ * 16 bytes, written only if the data XORs to a fixed pattern.  Returns the
+ * bytes one launch reads (each slice rounded down to whole 8 KB runs per
+ * wave) and the average launch duration; synchronises.  DSI_EINVAL for null
+ * pointers, a misaligned buffer, rounds < 1, slices < 1, workgroups outside
+ * 0..4096 or slices too small for 16 MiB and an 8 KB run per wave; DSI_EHIP
+ * if a launch or event fails. */
 dsi_status dsi_profile_stream(const void* d_buf, uint64_t bytes, int32_t slices, int32_t nontemporal,
-                              int32_t rounds, void* d_sink, uint64_t* bytes_per_launch, double* avg_ms);
+                              int32_t workgroups, int32_t rounds, void* d_sink, uint64_t* bytes_per_launch,
+                              double* avg_ms);
 
 /* Thread-local description of the last error. */
 const char* dsi_last_error(void);

@@ -368,12 +368,14 @@ hipError_t launch_kv_poison(int kv_bf16, void* kc, void* vc, size_t layer_stride
   return hipGetLastError();
 }
 
-hipError_t launch_stream_read(const void* buf, size_t per_wave_vec, int nontemporal, void* sink, hipStream_t s) {
+hipError_t launch_stream_read(const void* buf, size_t per_wave_vec, int workgroups, int nontemporal, void* sink,
+                              hipStream_t s) {
+  if (workgroups < 1 || workgroups > kStreamMaxWorkgroups) return hipErrorInvalidValue;
   if (nontemporal)
-    hipLaunchKernelGGL(k_stream_read<1>, dim3(kStreamWorkgroups), dim3(512), 0, s, (const u32x4*)buf, per_wave_vec,
+    hipLaunchKernelGGL(k_stream_read<1>, dim3(workgroups), dim3(512), 0, s, (const u32x4*)buf, per_wave_vec,
                        (u32x4*)sink);
   else
-    hipLaunchKernelGGL(k_stream_read<0>, dim3(kStreamWorkgroups), dim3(512), 0, s, (const u32x4*)buf, per_wave_vec,
+    hipLaunchKernelGGL(k_stream_read<0>, dim3(workgroups), dim3(512), 0, s, (const u32x4*)buf, per_wave_vec,
                        (u32x4*)sink);
   return hipGetLastError();
 }

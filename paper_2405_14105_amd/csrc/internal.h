@@ -320,8 +320,10 @@ hipError_t launch_kv_copy(int to_cache, int kv_bf16, void* kc, void* vc, int n_k
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
 // streaming read of kStreamWorkgroups x 8 waves, each over per_wave_vec
 // 16-byte vectors of buf (diagnostics: dsi_profile_stream)
-constexpr int kStreamWorkgroups = 256;
-hipError_t launch_stream_read(const void* buf, size_t per_wave_vec, int nontemporal, void* sink, hipStream_t s);
+constexpr int kStreamWorkgroups = 256;      // default grid
+constexpr int kStreamMaxWorkgroups = 4096;
+hipError_t launch_stream_read(const void* buf, size_t per_wave_vec, int workgroups, int nontemporal, void* sink,
+                              hipStream_t s);
 // NaN into rows [lens[window], maxlen) of every layer's K and V of one window
 // (kc / vc: the window's layer-0 base; layers layer_stride elements apart)
 hipError_t launch_kv_poison(int kv_bf16, void* kc, void* vc, size_t layer_stride, int n_layers, int n_kv, int hd,

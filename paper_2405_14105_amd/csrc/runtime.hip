@@ -1298,12 +1298,16 @@ dsi_status dsi_profile_end(dsi_model* m, int32_t* launches, double* total_ms) {
 }
 
 dsi_status dsi_profile_stream(const void* d_buf, uint64_t bytes, int32_t slices, int32_t nontemporal,
-                              int32_t rounds, void* d_sink, uint64_t* bytes_per_launch, double* avg_ms) {
+                              int32_t workgroups, int32_t rounds, void* d_sink, uint64_t* bytes_per_launch,
+                              double* avg_ms) {
   if (!d_buf || !d_sink || !bytes_per_launch || !avg_ms || rounds < 1 || slices < 1)
     return fail(DSI_EINVAL, "bad argument");
+  if (workgroups < 0 || workgroups > kStreamMaxWorkgroups)
+    return fail(DSI_EINVAL, "workgroups must be 0 (default %d) or 1..%d", kStreamWorkgroups, kStreamMaxWorkgroups);
   if (((uintptr_t)d_buf & 15) != 0) return fail(DSI_EINVAL, "buffer not 16-byte aligned");
+  const int wgs = workgroups ? workgroups : kStreamWorkgroups;
   const uint64_t slice = bytes / (uint64_t)slices;
-  const uint64_t waves = (uint64_t)kStreamWorkgroups * 8;
+  const uint64_t waves = (uint64_t)wgs * 8;
   const uint64_t run = slice / waves / 8192 * 8192;   // bytes per wave: whole rings of 8 x 1 KB
   if (run < 8192 || slice < (16ull << 20)) return fail(DSI_EINVAL, "slices must hold at least 16 MiB");
   const size_t per_wave_vec = (size_t)(run / 16);
@@ -1312,7 +1316,7 @@ dsi_status dsi_profile_stream(const void* d_buf, uint64_t bytes, int32_t slices,
   HIP_TRY(hipEventCreate(&e1));
   dsi_status st = DSI_OK;
   auto go = [&](int r) -> hipError_t {
-    return launch_stream_read((const char*)d_buf + (size_t)(r % slices) * slice, per_wave_vec, nontemporal,
+    return launch_stream_read((const char*)d_buf + (size_t)(r % slices) * slice, per_wave_vec, wgs, nontemporal,
                               d_sink, nullptr);
   };
   hipError_t e = go(0);   // warm-up

@@ -101,7 +101,7 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         "dsi_profile_end": ([P, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_double)], I32),
         "dsi_profile_kernel": ([P, P, I32, I32, ctypes.POINTER(ctypes.c_int32),
                                 ctypes.POINTER(ctypes.c_double)], I32),
-        "dsi_profile_stream": ([P, ctypes.c_uint64, I32, I32, I32, P, ctypes.POINTER(ctypes.c_uint64),
+        "dsi_profile_stream": ([P, ctypes.c_uint64, I32, I32, I32, I32, P, ctypes.POINTER(ctypes.c_uint64),
                                 ctypes.POINTER(ctypes.c_double)], I32),
         "dsi_last_error": ([], ctypes.c_char_p),
     }
@@ -246,13 +246,15 @@ def dsi_profile_kernel(model: int, kv: int, kernel_class: int, rounds: int = 3):
     return n.value, t.value
 
 
-def dsi_profile_stream(d_buf, nbytes: int, slices: int, nontemporal: bool, rounds: int, d_sink):
+def dsi_profile_stream(d_buf, nbytes: int, slices: int, nontemporal: bool, rounds: int, d_sink,
+                       workgroups: int = 0):
     """Returns (bytes per launch, avg_ms) of the library's streaming read over
-    `slices` slices of the device buffer d_buf, one per launch in turn."""
+    `slices` slices of the device buffer d_buf, one per launch in turn, with
+    `workgroups` workgroups of 8 waves (0: the default 256)."""
     b = ctypes.c_uint64()
     t = ctypes.c_double()
-    _check(load().dsi_profile_stream(_ptr(d_buf), nbytes, slices, int(bool(nontemporal)), rounds, _ptr(d_sink),
-                                     ctypes.byref(b), ctypes.byref(t)))
+    _check(load().dsi_profile_stream(_ptr(d_buf), nbytes, slices, int(bool(nontemporal)), workgroups, rounds,
+                                     _ptr(d_sink), ctypes.byref(b), ctypes.byref(t)))
     return b.value, t.value
 
 

@@ -111,11 +111,15 @@ int main(void) {
   expect("profile_end null", dsi_profile_end(NULL, &launches, &ms), DSI_EINVAL);
   expect("profile_kernel null", dsi_profile_kernel(NULL, NULL, DSI_K_QKV, 1, &launches, &ms), DSI_EINVAL);
   uint64_t nb = 0;
-  expect("profile_stream null buffer", dsi_profile_stream(NULL, 1 << 30, 1, 0, 1, P, &nb, &ms), DSI_EINVAL);
-  expect("profile_stream misaligned", dsi_profile_stream((const char*)P + 4, 1 << 30, 1, 0, 1, P, &nb, &ms),
+  expect("profile_stream null buffer", dsi_profile_stream(NULL, 1 << 30, 1, 0, 0, 1, P, &nb, &ms), DSI_EINVAL);
+  expect("profile_stream misaligned", dsi_profile_stream((const char*)P + 4, 1 << 30, 1, 0, 0, 1, P, &nb, &ms),
          DSI_EINVAL);
-  expect("profile_stream small slices", dsi_profile_stream(P, 32 << 20, 4, 0, 1, P, &nb, &ms), DSI_EINVAL);
-  expect("profile_stream zero rounds", dsi_profile_stream(P, 1 << 30, 1, 0, 0, P, &nb, &ms), DSI_EINVAL);
+  expect("profile_stream small slices", dsi_profile_stream(P, 32 << 20, 4, 0, 0, 1, P, &nb, &ms), DSI_EINVAL);
+  expect("profile_stream zero rounds", dsi_profile_stream(P, 1 << 30, 1, 0, 0, 0, P, &nb, &ms), DSI_EINVAL);
+  expect("profile_stream negative workgroups", dsi_profile_stream(P, 1 << 30, 1, 0, -1, 1, P, &nb, &ms),
+         DSI_EINVAL);
+  expect("profile_stream too many workgroups", dsi_profile_stream(P, 1 << 30, 1, 0, 4097, 1, P, &nb, &ms),
+         DSI_EINVAL);
 
   /* accept/reject: host validation of the batch shape and arguments */
   expect("accept zero windows", dsi_accept(NULL, 0, 3, 100, fdummy, dummy, fdummy, fdummy, 1.f, 0, dummy, dummy),

@@ -15,13 +15,19 @@ def test_stream_read_rate_and_argument_checks():
     sink = torch.zeros(16, dtype=torch.uint8, device=dev)
     torch.cuda.synchronize()
     rates = {}
-    for nt in (False, True):
-        nb, ms = dsi.dsi_profile_stream(buf, slice_bytes * slices, slices, nt, 8, sink)
-        # each slice rounded down to whole 8 KB runs of the 2048 waves
-        assert slice_bytes - 2048 * 8192 < nb <= slice_bytes and nb % (2048 * 8192) == 0
-        rates[nt] = nb / (ms * 1e-3) / 1e9
-        print(f"nontemporal={nt}: {nb >> 20} MiB per launch, {ms * 1e3:.1f} us, {rates[nt]:.0f} GB/s")
-        assert 500.0 < rates[nt] < 8000.0     # below the HBM peak: every launch reads HBM
+    for nt, wg in ((False, 0), (True, 0), (True, 192), (True, 32)):
+        nb, ms = dsi.dsi_profile_stream(buf, slice_bytes * slices, slices, nt, 8, sink, workgroups=wg)
+        # each slice rounded down to whole 8 KB runs of the launch's waves
+        waves = (wg or 256) * 8
+        assert slice_bytes - waves * 8192 < nb <= slice_bytes and nb % (waves * 8192) == 0
+        rates[nt, wg] = nb / (ms * 1e-3) / 1e9
+        print(f"nontemporal={nt} workgroups={wg or 256}: {nb >> 20} MiB per launch, {ms * 1e3:.1f} us, "
+              f"{rates[nt, wg]:.0f} GB/s")
+        assert 500.0 < rates[nt, wg] < 8000.0     # below the HBM peak: every launch reads HBM
+    for bad in (-1, 4097):                         # workgroups outside 0..4096
+        with pytest.raises(dsi.DsiError) as ei:
+            dsi.dsi_profile_stream(buf, slice_bytes, 1, False, 1, sink, workgroups=bad)
+        assert ei.value.status == dsi.DSI_EINVAL
     with pytest.raises(dsi.DsiError) as ei:    # misaligned buffer
         dsi.dsi_profile_stream(buf.data_ptr() + 4, slice_bytes, 1, False, 1, sink)
     assert ei.value.status == dsi.DSI_EINVAL

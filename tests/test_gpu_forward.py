@@ -44,6 +44,12 @@ CASES = [
     # one key chunk of three steps per wave (no combine launch)
     ("o_ring_hd64", 700, 5),
     ("o_ring_hd128", 300, 10),
+    # a 32-key step whose last key is position len + 1 (row 0's next key:
+    # it must take the masked path) and one ending exactly at len (all its
+    # keys visible to every row: mask-free); with ~64 keys a wrongly visible
+    # key would carry ~1/64 of row 0's attention
+    ("o_ring_hd128", 62, 10),
+    ("o_ring_hd128", 63, 10),
     # a 9000-wide FFN: 161 gate/up ring workgroups, and the down projection
     # split four ways (the small shapes above split it at most twice)
     ("ring_wide_ff", 200, 6),
